@@ -1,0 +1,126 @@
+/*
+ * kvpop.h -- C ABI of the KVpop future-attention target library (gfx950 / MI355X).
+ *
+ * The library computes, for every key position t and every query head, the dense
+ * causal softmax probability mass that query positions at or after t place on key
+ * t (KVpop, Sec. 3.1 eq. future_mass_per_group without the 1/N_t factor; App. B.1
+ * eq. group_future_mass_app; App. D.1 eq. future_mass_app), without materialising
+ * the T x T attention map. It works in two passes on the caller's stream:
+ *
+ *   pass 1  kvpop_row_lse              LSE_d = log sum_{t <= d} exp l(d, t)
+ *           (App. D.1 eq. dense_lse_app; the per-query normaliser that App. D.4
+ *            step 1 takes from the main attention pass)
+ *   pass 2  kvpop_future_attn_from_lse out_t = sum_{d in band(t)} exp(l(d, t) - LSE_d)
+ *           (App. D.1 eq. future_mass_app; App. D.4 steps 2-4 evaluate the same
+ *            sum as the log-sum-exp of a transposed attention pass, App. D.2)
+ *   both    kvpop_future_attn_target   pass 1 then pass 2
+ *
+ * with the logit (App. D.1 eq. dense_logit_app, plus an optional per-key bias)
+ *
+ *   l(d, t) = scale * <Q[b, qh, d, :], K[b, qh / G, t, :]> + key_bias[t],  t <= d,
+ *
+ * and band(t) = { d : t + window <= d <= min(T - 1, t + horizon) } (horizon < 0:
+ * up to T - 1). The paper's protected window w is `window`; its finite lookahead L
+ * (App. B.2) is horizon = w + L. The paper's full-future target is window = w,
+ * horizon = -1; window = 0 includes the diagonal d = t.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Shapes: B = batch, Hq = query heads, Hkv = KV heads (Hq % Hkv == 0,
+ *    G = Hq / Hkv), T = sequence length, D = head dim (64 or 128).
+ *  - Q is bf16 [B, Hq, T, D] and K is bf16 [B, Hkv, T, D], both contiguous
+ *    row-major device memory (bf16 = IEEE binary32 with the low 16 bits dropped).
+ *    Query head qh reads KV head qh / G (contiguous query-head groups).
+ *  - key_bias is an optional fp32 [T] device array (NULL = no bias), shared by all
+ *    batch rows and heads. Values may be -INFINITY (key never attended). Finite
+ *    values must be >= -80: pass 2 factors exp(key_bias[t]) out of each key's sum,
+ *    and below that bound the factored sum may overflow.
+ *  - lse is fp32 [B, Hq, T] holding natural-log normalisers; out is fp32
+ *    [B, Hq, T] holding the linear (not log) unnormalised future mass. Keys whose
+ *    band is empty (t + window > T - 1) get exactly 0.
+ *  - All pointers are device pointers that the caller allocates and owns; the
+ *    library allocates nothing and keeps no state between calls. Every base
+ *    pointer must be 16-byte aligned. Outputs are fully overwritten (no
+ *    pre-zeroing needed) and must not alias any input or each other.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream). Every
+ *    call only enqueues work: it returns once the kernels are launched, and the
+ *    caller must keep all buffers alive until the stream has passed them.
+ *  - Arguments are validated before anything is launched; on error nothing is
+ *    enqueued and no output is touched.
+ *  - Thread safety: calls may be made concurrently from several host threads;
+ *    the error text of KVPOP_EHIP is kept per thread.
+ */
+#ifndef KVPOP_H
+#define KVPOP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KVPOP_ABI_VERSION 1
+
+/* Status codes returned by every entry point. */
+enum {
+  KVPOP_OK = 0,
+  KVPOP_EINVAL = 1,       /* NULL required pointer, non-positive dimension, Hq % Hkv != 0,
+                             window < 0, 0 <= horizon < window, scale not finite and > 0,
+                             or a size whose element count overflows int64 */
+  KVPOP_EUNSUPPORTED = 2, /* head_dim not in {64, 128}, a base pointer not 16-byte
+                             aligned, or T above KVPOP_MAX_SEQ_LEN */
+  KVPOP_EHIP = 3          /* the HIP runtime reported an error while launching;
+                             kvpop_strerror(KVPOP_EHIP) then returns its text */
+};
+
+#define KVPOP_MAX_SEQ_LEN (1 << 24)
+
+/* Problem dimensions (see the conventions above). scale is the softmax scale of
+ * eq. dense_logit_app, normally 1 / sqrt(head_dim). */
+typedef struct kvpop_dims {
+  int32_t batch;      /* B   >= 1 */
+  int32_t n_q_heads;  /* Hq  >= 1 */
+  int32_t n_kv_heads; /* Hkv >= 1, Hq % Hkv == 0 */
+  int32_t seq_len;    /* T   >= 1 */
+  int32_t head_dim;   /* D   in {64, 128} */
+  float scale;        /* > 0 and finite */
+} kvpop_dims;
+
+/* Pass 1 -- dense causal row log-normaliser (App. D.1 eq. dense_lse_app):
+ *   lse[b, qh, d] = log sum_{t=0}^{d} exp(l(d, t)).
+ * q: bf16 [B,Hq,T,D]; k: bf16 [B,Hkv,T,D]; key_bias: fp32 [T] or NULL;
+ * lse: fp32 [B,Hq,T] output. */
+int kvpop_row_lse(const kvpop_dims* dims, const void* q, const void* k, const float* key_bias,
+                  float* lse, void* stream);
+
+/* Pass 2 -- future mass from a caller-supplied normaliser (App. D.1 eq.
+ * future_mass_app, App. D.2):
+ *   out[b, qh, t] = sum_{d in band(t)} exp(l(d, t) - lse[b, qh, d]).
+ * lse is normally the output of kvpop_row_lse on the same q, k, key_bias, which
+ * makes every summand a probability (<= 1). With any other normaliser (e.g. the
+ * sparse one of App. D.3) the caller must ensure l(d, t) - lse[d] stays below
+ * about 88 for admissible pairs, or the sums overflow to +inf.
+ * window >= 0; horizon < 0 (unbounded) or horizon >= window. out: fp32 [B,Hq,T]. */
+int kvpop_future_attn_from_lse(const kvpop_dims* dims, const void* q, const void* k,
+                               const float* key_bias, const float* lse, int32_t window,
+                               int32_t horizon, float* out, void* stream);
+
+/* Both passes: kvpop_row_lse into lse_ws, then kvpop_future_attn_from_lse from it.
+ * lse_ws: caller-allocated fp32 [B,Hq,T]; it holds the dense LSE on completion. */
+int kvpop_future_attn_target(const kvpop_dims* dims, const void* q, const void* k,
+                             const float* key_bias, int32_t window, int32_t horizon,
+                             float* lse_ws, float* out, void* stream);
+
+/* Human-readable text for a status code. For KVPOP_EHIP it is the HIP runtime's
+ * message for the last failure on the calling thread. Never returns NULL; the
+ * string stays valid until the next library call on the same thread. */
+const char* kvpop_strerror(int status);
+
+/* KVPOP_ABI_VERSION of the loaded library. */
+int kvpop_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVPOP_H */

@@ -1,0 +1,32 @@
+"""fp64 CPU oracle for the KVpop future-attention target.
+
+TEST INFRASTRUCTURE ONLY. Only the tests, the smoke check and the benchmark's CPU
+baseline may import this package. The library's GPU path never calls it, and the
+two share no code: the oracle decodes bf16 bit patterns itself and evaluates the
+paper's definitions directly in float64.
+
+What it computes (paper, App. D.1, eqs. dense_logit_app .. future_mass_app):
+
+* logits   l(d, t) = scale * <q_d, k_t> + bias_t           (t <= d, causal)
+* LSE_d    = log sum_{t <= d} exp l(d, t)                   (row log-normaliser)
+* p_{d->t} = exp(l(d, t) - LSE_d)                           (causal probability)
+* m_t      = sum_{d = t + window}^{min(T-1, t + horizon)} p_{d->t}
+             (unnormalised future mass; horizon < 0 means up to T-1)
+
+plus the transposed log-space form of App. D.2 (eq. future_mass_lse_app), used as an
+independent cross-check of the same quantity.
+
+Every function here is pinned by tests against closed forms, hand enumeration and
+brute force (tests/test_oracle_pins.py); no function is "parity unpinned".
+"""
+from .future_mass import (  # noqa: F401
+    bf16_bits_to_f64,
+    causal_logits,
+    future_mass,
+    future_mass_blocked,
+    future_mass_columns,
+    future_mass_transposed,
+    row_lse,
+    row_lse_blocked,
+    row_lse_rows,
+)
