@@ -1,0 +1,193 @@
+"""KVpop future-attention target on MI355X (gfx950).
+
+A thin ctypes binding over the in-tree ``libkvpop.so`` (C ABI in ``include/kvpop.h``).
+Every function here only marshals arguments: it checks tensor placement, dtype and
+layout, derives the dimensions, allocates outputs with PyTorch when the caller
+passes none, and calls the C entry point of the same name on the current HIP
+stream. All arithmetic runs in the library's HIP kernels; there is no fallback.
+
+Quantities (KVpop App. D.1): for query head qh and key position t,
+
+    lse[b, qh, d] = log sum_{t <= d} exp(scale <q_d, k_t> + bias_t)       (pass 1)
+    out[b, qh, t] = sum_{d = t + window}^{min(T - 1, t + horizon)}
+                    exp(scale <q_d, k_t> + bias_t - lse[b, qh, d])       (pass 2)
+
+with query head qh reading KV head qh // (Hq // Hkv); horizon < 0 = no limit.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+__all__ = [
+    "KVPOP_OK", "KVPOP_EINVAL", "KVPOP_EUNSUPPORTED", "KVPOP_EHIP", "KvpopDims", "KvpopError",
+    "lib", "lib_path", "kvpop_row_lse", "kvpop_future_attn_from_lse", "kvpop_future_attn_target",
+    "kvpop_strerror", "kvpop_abi_version",
+]
+
+KVPOP_OK = 0
+KVPOP_EINVAL = 1
+KVPOP_EUNSUPPORTED = 2
+KVPOP_EHIP = 3
+ABI_VERSION = 1
+
+_PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+_LIB: Optional[ctypes.CDLL] = None
+
+
+class KvpopDims(ctypes.Structure):
+    """Mirror of ``kvpop_dims`` in include/kvpop.h."""
+    _fields_ = [
+        ("batch", ctypes.c_int32),
+        ("n_q_heads", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32),
+        ("seq_len", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("scale", ctypes.c_float),
+    ]
+
+
+class KvpopError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__("%s failed with status %d: %s" % (where, status, kvpop_strerror(status)))
+        self.status = status
+
+
+def lib_path() -> str:
+    return os.environ.get("KVPOP_LIB", os.path.join(_PKG_DIR, "libkvpop.so"))
+
+
+def lib() -> ctypes.CDLL:
+    """Load the built library (raises if it has not been built)."""
+    global _LIB
+    if _LIB is None:
+        path = lib_path()
+        if not os.path.exists(path):
+            raise RuntimeError("libkvpop.so not found at %s: build it with "
+                               "`python -m paper_2607_05061_amd.build`" % path)
+        L = ctypes.CDLL(path)
+        P, I32, F = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float
+        D = ctypes.POINTER(KvpopDims)
+        L.kvpop_row_lse.argtypes = [D, P, P, P, P, P]
+        L.kvpop_row_lse.restype = ctypes.c_int
+        L.kvpop_future_attn_from_lse.argtypes = [D, P, P, P, P, I32, I32, P, P]
+        L.kvpop_future_attn_from_lse.restype = ctypes.c_int
+        L.kvpop_future_attn_target.argtypes = [D, P, P, P, I32, I32, P, P, P]
+        L.kvpop_future_attn_target.restype = ctypes.c_int
+        L.kvpop_strerror.argtypes = [ctypes.c_int]
+        L.kvpop_strerror.restype = ctypes.c_char_p
+        L.kvpop_abi_version.argtypes = []
+        L.kvpop_abi_version.restype = ctypes.c_int
+        if L.kvpop_abi_version() != ABI_VERSION:
+            raise RuntimeError("libkvpop ABI version %d, binding expects %d" % (L.kvpop_abi_version(), ABI_VERSION))
+        _LIB = L
+    return _LIB
+
+
+def kvpop_strerror(status: int) -> str:
+    return lib().kvpop_strerror(int(status)).decode()
+
+
+def kvpop_abi_version() -> int:
+    return int(lib().kvpop_abi_version())
+
+
+# ---------------------------------------------------------------------------
+# torch-tensor marshalling
+# ---------------------------------------------------------------------------
+
+def _torch():
+    import torch  # noqa: WPS433 (PyTorch only provides device memory and streams)
+    return torch
+
+
+def _dims(q, k, scale: float) -> KvpopDims:
+    if q.dim() != 4 or k.dim() != 4:
+        raise ValueError("q must be [B, Hq, T, D] and k [B, Hkv, T, D]")
+    B, Hq, T, D = q.shape
+    if k.shape[0] != B or k.shape[2] != T or k.shape[3] != D:
+        raise ValueError("q %s and k %s disagree on B, T or D" % (tuple(q.shape), tuple(k.shape)))
+    return KvpopDims(B, Hq, k.shape[1], T, D, float(scale))
+
+
+def _check_tensor(x, name: str, dtype, device):
+    torch = _torch()
+    if not isinstance(x, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if x.device.type != "cuda" or (device is not None and x.device != device):
+        raise ValueError("%s must be on the GPU device of q" % name)
+    if x.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, x.dtype))
+    if not x.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+
+
+def _stream_ptr(stream, device) -> int:
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    return int(s.cuda_stream)
+
+
+def _prep_inputs(q, k, key_bias):
+    torch = _torch()
+    _check_tensor(q, "q", torch.bfloat16, None)
+    _check_tensor(k, "k", torch.bfloat16, q.device)
+    if key_bias is not None:
+        _check_tensor(key_bias, "key_bias", torch.float32, q.device)
+        if key_bias.dim() != 1 or key_bias.shape[0] != q.shape[2]:
+            raise ValueError("key_bias must be [T]")
+    return q.data_ptr(), k.data_ptr(), (key_bias.data_ptr() if key_bias is not None else None)
+
+
+def _prep_out(x, name, shape, device):
+    torch = _torch()
+    if x is None:
+        return torch.empty(shape, dtype=torch.float32, device=device)
+    _check_tensor(x, name, torch.float32, device)
+    if tuple(x.shape) != tuple(shape):
+        raise ValueError("%s must have shape %s" % (name, tuple(shape)))
+    return x
+
+
+def kvpop_row_lse(q, k, scale: float, key_bias=None, lse=None, stream=None):
+    """Pass 1: dense causal row log-normaliser, fp32 [B, Hq, T] (eq. dense_lse_app)."""
+    d = _dims(q, k, scale)
+    qp, kp, bp = _prep_inputs(q, k, key_bias)
+    lse = _prep_out(lse, "lse", (d.batch, d.n_q_heads, d.seq_len), q.device)
+    st = lib().kvpop_row_lse(ctypes.byref(d), qp, kp, bp, lse.data_ptr(), _stream_ptr(stream, q.device))
+    if st != KVPOP_OK:
+        raise KvpopError(st, "kvpop_row_lse")
+    return lse
+
+
+def kvpop_future_attn_from_lse(q, k, lse, scale: float, window: int = 0, horizon: int = -1, key_bias=None,
+                               out=None, stream=None):
+    """Pass 2: per-key future mass from a given normaliser, fp32 [B, Hq, T] (eq. future_mass_app)."""
+    torch = _torch()
+    d = _dims(q, k, scale)
+    qp, kp, bp = _prep_inputs(q, k, key_bias)
+    _check_tensor(lse, "lse", torch.float32, q.device)
+    if tuple(lse.shape) != (d.batch, d.n_q_heads, d.seq_len):
+        raise ValueError("lse must be [B, Hq, T]")
+    out = _prep_out(out, "out", (d.batch, d.n_q_heads, d.seq_len), q.device)
+    st = lib().kvpop_future_attn_from_lse(ctypes.byref(d), qp, kp, bp, lse.data_ptr(), int(window), int(horizon),
+                                          out.data_ptr(), _stream_ptr(stream, q.device))
+    if st != KVPOP_OK:
+        raise KvpopError(st, "kvpop_future_attn_from_lse")
+    return out
+
+
+def kvpop_future_attn_target(q, k, scale: float, window: int = 0, horizon: int = -1, key_bias=None,
+                             lse_ws=None, out=None, stream=None) -> Tuple["object", "object"]:
+    """Both passes; returns (out, lse) where lse is the dense normaliser of pass 1."""
+    d = _dims(q, k, scale)
+    qp, kp, bp = _prep_inputs(q, k, key_bias)
+    shape = (d.batch, d.n_q_heads, d.seq_len)
+    lse_ws = _prep_out(lse_ws, "lse_ws", shape, q.device)
+    out = _prep_out(out, "out", shape, q.device)
+    st = lib().kvpop_future_attn_target(ctypes.byref(d), qp, kp, bp, int(window), int(horizon), lse_ws.data_ptr(),
+                                        out.data_ptr(), _stream_ptr(stream, q.device))
+    if st != KVPOP_OK:
+        raise KvpopError(st, "kvpop_future_attn_target")
+    return out, lse_ws

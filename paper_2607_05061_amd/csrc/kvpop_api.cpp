@@ -1,0 +1,177 @@
+// C ABI of the KVpop future-attention target library: argument validation, error
+// reporting and dispatch to the gfx950 kernels. The semantics of every entry point
+// are specified in include/kvpop.h.
+#include "kvpop.h"
+
+#include <hip/hip_runtime_api.h>
+
+#include <cmath>
+#include <cstdint>
+#include <string>
+
+#include "kvpop_internal.h"
+
+namespace {
+
+thread_local std::string g_err_text;
+
+struct Sizes {
+  int64_t q_elems, k_elems, row_elems;  // Q, K and [B, Hq, T] element counts
+};
+
+bool mul_ok(int64_t a, int64_t b, int64_t* r) {
+  if (a != 0 && b > INT64_MAX / a) return false;
+  *r = a * b;
+  return true;
+}
+
+int check_dims(const kvpop_dims* d, Sizes* sz) {
+  if (!d) return KVPOP_EINVAL;
+  if (d->batch < 1 || d->n_q_heads < 1 || d->n_kv_heads < 1 || d->seq_len < 1 || d->head_dim < 1)
+    return KVPOP_EINVAL;
+  if (d->n_q_heads % d->n_kv_heads != 0) return KVPOP_EINVAL;
+  if (!std::isfinite(d->scale) || !(d->scale > 0.f)) return KVPOP_EINVAL;
+  if (d->head_dim != 64 && d->head_dim != 128) return KVPOP_EUNSUPPORTED;
+  if (d->seq_len > KVPOP_MAX_SEQ_LEN) return KVPOP_EUNSUPPORTED;
+  int64_t bh, bkh, t;
+  if (!mul_ok(d->batch, d->n_q_heads, &bh) || !mul_ok(bh, d->seq_len, &sz->row_elems) ||
+      !mul_ok(sz->row_elems, d->head_dim, &sz->q_elems) || !mul_ok(d->batch, d->n_kv_heads, &bkh) ||
+      !mul_ok(bkh, d->seq_len, &t) || !mul_ok(t, d->head_dim, &sz->k_elems) ||
+      sz->q_elems > INT64_MAX / 4)
+    return KVPOP_EINVAL;
+  // Grid sizes stay below 2^31 workgroups: at most B * Hq * ceil(T / 32) of them.
+  if (sz->row_elems / 32 + bh > INT32_MAX) return KVPOP_EUNSUPPORTED;
+  return KVPOP_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool overlap(const void* a, int64_t abytes, const void* b, int64_t bbytes) {
+  if (!a || !b) return false;
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
+  return a0 < b0 + (uintptr_t)bbytes && b0 < a0 + (uintptr_t)abytes;
+}
+
+int check_band(int32_t window, int32_t horizon) {
+  if (window < 0) return KVPOP_EINVAL;
+  if (horizon >= 0 && horizon < window) return KVPOP_EINVAL;
+  return KVPOP_OK;
+}
+
+int hip_status(int e) {
+  if (e == 0) return KVPOP_OK;
+  g_err_text = std::string("HIP error: ") + hipGetErrorString(static_cast<hipError_t>(e));
+  return KVPOP_EHIP;
+}
+
+kvpop::Launch make_launch(const kvpop_dims* d, const void* q, const void* k, const float* bias, void* stream) {
+  kvpop::Launch L{};
+  L.q = static_cast<const uint16_t*>(q);
+  L.k = static_cast<const uint16_t*>(k);
+  L.bias = bias;
+  L.B = d->batch;
+  L.Hq = d->n_q_heads;
+  L.Hkv = d->n_kv_heads;
+  L.T = d->seq_len;
+  L.D = d->head_dim;
+  L.scale = d->scale;
+  L.stream = stream;
+  return L;
+}
+
+// Validation shared by every entry point for the inputs q, k, key_bias.
+int check_inputs(const kvpop_dims* d, const void* q, const void* k, const float* bias, Sizes* sz) {
+  int st = check_dims(d, sz);
+  if (st != KVPOP_OK) return st;
+  if (!q || !k) return KVPOP_EINVAL;
+  if (!aligned16(q) || !aligned16(k) || (bias && !aligned16(bias))) return KVPOP_EUNSUPPORTED;
+  return KVPOP_OK;
+}
+
+// An output of `bytes` bytes must not overlap q, k, bias or `other`.
+int check_output(const void* out, int64_t bytes, const Sizes& sz, const kvpop_dims* d, const void* q,
+                 const void* k, const float* bias, const void* other, int64_t other_bytes) {
+  if (!out) return KVPOP_EINVAL;
+  if (!aligned16(out)) return KVPOP_EUNSUPPORTED;
+  if (overlap(out, bytes, q, sz.q_elems * 2) || overlap(out, bytes, k, sz.k_elems * 2) ||
+      overlap(out, bytes, bias, (int64_t)d->seq_len * 4) || overlap(out, bytes, other, other_bytes))
+    return KVPOP_EINVAL;
+  return KVPOP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int kvpop_abi_version(void) { return KVPOP_ABI_VERSION; }
+
+const char* kvpop_strerror(int status) {
+  switch (status) {
+    case KVPOP_OK:
+      return "success";
+    case KVPOP_EINVAL:
+      return "invalid argument (null pointer, bad dimension, Hq % Hkv != 0, bad scale, bad window/horizon, "
+             "or overlapping buffers)";
+    case KVPOP_EUNSUPPORTED:
+      return "unsupported configuration (head_dim not 64/128, pointer not 16-byte aligned, or size limit)";
+    case KVPOP_EHIP:
+      return g_err_text.empty() ? "HIP runtime error" : g_err_text.c_str();
+    default:
+      return "unknown status code";
+  }
+}
+
+int kvpop_row_lse(const kvpop_dims* dims, const void* q, const void* k, const float* key_bias, float* lse,
+                  void* stream) {
+  Sizes sz;
+  int st = check_inputs(dims, q, k, key_bias, &sz);
+  if (st != KVPOP_OK) return st;
+  st = check_output(lse, sz.row_elems * 4, sz, dims, q, k, key_bias, nullptr, 0);
+  if (st != KVPOP_OK) return st;
+  kvpop::Launch L = make_launch(dims, q, k, key_bias, stream);
+  L.out = lse;
+  return hip_status(kvpop::launch_row_lse(L));
+}
+
+int kvpop_future_attn_from_lse(const kvpop_dims* dims, const void* q, const void* k, const float* key_bias,
+                               const float* lse, int32_t window, int32_t horizon, float* out, void* stream) {
+  Sizes sz;
+  int st = check_inputs(dims, q, k, key_bias, &sz);
+  if (st != KVPOP_OK) return st;
+  if (!lse) return KVPOP_EINVAL;
+  if (!aligned16(lse)) return KVPOP_EUNSUPPORTED;
+  st = check_band(window, horizon);
+  if (st != KVPOP_OK) return st;
+  st = check_output(out, sz.row_elems * 4, sz, dims, q, k, key_bias, lse, sz.row_elems * 4);
+  if (st != KVPOP_OK) return st;
+  kvpop::Launch L = make_launch(dims, q, k, key_bias, stream);
+  L.lse = lse;
+  L.out = out;
+  L.window = window;
+  L.horizon = horizon;
+  return hip_status(kvpop::launch_future_mass(L));
+}
+
+int kvpop_future_attn_target(const kvpop_dims* dims, const void* q, const void* k, const float* key_bias,
+                             int32_t window, int32_t horizon, float* lse_ws, float* out, void* stream) {
+  Sizes sz;
+  int st = check_inputs(dims, q, k, key_bias, &sz);
+  if (st != KVPOP_OK) return st;
+  st = check_band(window, horizon);
+  if (st != KVPOP_OK) return st;
+  st = check_output(lse_ws, sz.row_elems * 4, sz, dims, q, k, key_bias, out, sz.row_elems * 4);
+  if (st != KVPOP_OK) return st;
+  st = check_output(out, sz.row_elems * 4, sz, dims, q, k, key_bias, lse_ws, sz.row_elems * 4);
+  if (st != KVPOP_OK) return st;
+  kvpop::Launch L = make_launch(dims, q, k, key_bias, stream);
+  L.out = lse_ws;
+  st = hip_status(kvpop::launch_row_lse(L));
+  if (st != KVPOP_OK) return st;
+  L.lse = lse_ws;
+  L.out = out;
+  L.window = window;
+  L.horizon = horizon;
+  return hip_status(kvpop::launch_future_mass(L));
+}
+
+}  // extern "C"

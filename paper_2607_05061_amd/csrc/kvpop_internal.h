@@ -1,0 +1,26 @@
+// Internal interface between the C ABI layer (kvpop_api.cpp) and the gfx950
+// kernels (kvpop_kernels.hip). Not part of the public ABI.
+#pragma once
+#include <stdint.h>
+
+namespace kvpop {
+
+// Launch description shared by both passes. All sizes already validated.
+struct Launch {
+  const uint16_t* q;   // bf16 [B, Hq, T, D]
+  const uint16_t* k;   // bf16 [B, Hkv, T, D]
+  const float* bias;   // fp32 [T] or nullptr
+  const float* lse;    // pass 2 input: fp32 [B, Hq, T]
+  float* out;          // pass 1: lse output; pass 2: future-mass output
+  int32_t B, Hq, Hkv, T, D;
+  float scale;
+  int32_t window;      // pass 2 only
+  int32_t horizon;     // pass 2 only; < 0 = unbounded
+  void* stream;        // hipStream_t
+};
+
+// Each returns 0 on success or the hipError_t of a failed launch.
+int launch_row_lse(const Launch& L);
+int launch_future_mass(const Launch& L);
+
+}  // namespace kvpop

@@ -1,0 +1,129 @@
+"""The C ABI library loads, exports every declared entry point, and rejects bad
+arguments with the documented status before launching anything (no GPU needed)."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import paper_2607_05061_amd as kv
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kvpop.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(kv.lib_path()),
+                                reason="libkvpop.so not built (python -m paper_2607_05061_amd.build)")
+
+
+def _declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(kvpop_\w+)\s*\(", src, flags=re.M)
+
+
+def test_header_declares_the_entry_points():
+    names = set(_declared_functions())
+    assert names == {"kvpop_row_lse", "kvpop_future_attn_from_lse", "kvpop_future_attn_target",
+                     "kvpop_strerror", "kvpop_abi_version"}
+
+
+def test_library_exports_every_declared_symbol():
+    L = kv.lib()
+    for name in _declared_functions():
+        assert hasattr(L, name), name
+        assert ctypes.cast(getattr(L, name), ctypes.c_void_p).value
+
+
+def test_abi_version_and_strerror():
+    assert kv.kvpop_abi_version() == 1
+    texts = {c: kv.kvpop_strerror(c) for c in (kv.KVPOP_OK, kv.KVPOP_EINVAL, kv.KVPOP_EUNSUPPORTED, kv.KVPOP_EHIP, 99)}
+    assert texts[kv.KVPOP_OK] == "success"
+    assert "invalid" in texts[kv.KVPOP_EINVAL]
+    assert "unsupported" in texts[kv.KVPOP_EUNSUPPORTED]
+    assert "HIP" in texts[kv.KVPOP_EHIP]
+    assert "unknown" in texts[99]
+    assert len(set(texts.values())) == 5
+
+
+# Fake device addresses: never dereferenced, because every call below must be
+# rejected during validation.
+A, B_, C_, D_, E_ = 0x10000000, 0x20000000, 0x30000000, 0x40000000, 0x50000000
+
+
+def _dims(B=1, Hq=4, Hkv=2, T=64, D=128, scale=0.125):
+    return kv.KvpopDims(B, Hq, Hkv, T, D, scale)
+
+
+def _lse(d, q=A, k=B_, bias=None, out=C_):
+    return kv.lib().kvpop_row_lse(ctypes.byref(d) if d is not None else None, q, k, bias, out, None)
+
+
+def _p2(d, q=A, k=B_, bias=None, lse=C_, w=0, h=-1, out=D_):
+    return kv.lib().kvpop_future_attn_from_lse(ctypes.byref(d) if d is not None else None, q, k, bias, lse, w, h, out,
+                                               None)
+
+
+def _tgt(d, q=A, k=B_, bias=None, w=0, h=-1, ws=C_, out=D_):
+    return kv.lib().kvpop_future_attn_target(ctypes.byref(d) if d is not None else None, q, k, bias, w, h, ws, out,
+                                             None)
+
+
+EINVAL, EUNS = kv.KVPOP_EINVAL, kv.KVPOP_EUNSUPPORTED
+
+
+@pytest.mark.parametrize("call", [_lse, _p2, _tgt])
+def test_bad_dims(call):
+    assert call(None) == EINVAL
+    for kw in (dict(B=0), dict(Hq=0), dict(Hkv=0), dict(T=0), dict(D=0), dict(B=-1), dict(T=-5)):
+        assert call(_dims(**kw)) == EINVAL, kw
+    assert call(_dims(Hq=6, Hkv=4)) == EINVAL
+    for s in (0.0, -0.1, math.inf, math.nan):
+        assert call(_dims(scale=s)) == EINVAL, s
+    for dd in (32, 96, 256, 80):
+        assert call(_dims(D=dd)) == EUNS, dd
+    assert call(_dims(T=(1 << 24) + 1)) == EUNS
+
+
+@pytest.mark.parametrize("call", [_lse, _p2, _tgt])
+def test_null_and_misaligned_pointers(call):
+    d = _dims()
+    assert call(d, q=None) == EINVAL
+    assert call(d, k=None) == EINVAL
+    assert call(d, q=A + 8) == EUNS
+    assert call(d, k=B_ + 2) == EUNS
+    assert call(d, bias=E_ + 4) == EUNS
+
+
+def test_output_pointer_checks():
+    d = _dims()
+    assert _lse(d, out=None) == EINVAL
+    assert _lse(d, out=C_ + 4) == EUNS
+    assert _p2(d, out=None) == EINVAL
+    assert _p2(d, lse=None) == EINVAL
+    assert _p2(d, lse=C_ + 8) == EUNS
+    assert _tgt(d, ws=None) == EINVAL
+    assert _tgt(d, out=None) == EINVAL
+
+
+def test_overlapping_buffers_rejected():
+    d = _dims()  # Q is 1*4*64*128*2 = 64 KiB
+    assert _lse(d, out=A + 4096) == EINVAL          # lse inside Q
+    assert _p2(d, out=C_) == EINVAL                # out == lse
+    assert _tgt(d, ws=D_, out=D_ + 16) == EINVAL    # out overlaps workspace
+    assert _p2(d, bias=E_, out=E_) == EINVAL        # out over the bias
+
+
+@pytest.mark.parametrize("call", [_p2, _tgt])
+def test_bad_bands(call):
+    d = _dims()
+    assert call(d, w=-1) == EINVAL
+    assert call(d, w=3, h=2) == EINVAL
+    assert call(d, w=5, h=0) == EINVAL
+
+
+def test_python_binding_rejects_cpu_tensors():
+    torch = pytest.importorskip("torch")
+    q = torch.zeros(1, 1, 4, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        kv.kvpop_row_lse(q, q, 0.125)

@@ -1,0 +1,318 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 oracle.
+
+Bar (per query head and key): |gpu - oracle| <= 2e-3 * oracle for every key whose
+query range is non-empty, exactly 0 for keys whose range is empty; the pass-1 LSE
+within 5e-4 absolute. Inputs are the same bf16 bit patterns on both sides, from
+the seeded generator in ``workload``.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import workload
+
+torch = pytest.importorskip("torch")
+import paper_2607_05061_amd as kv  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+REL = 2e-3
+LSE_ABS = 5e-4
+
+
+def _dev(bits: np.ndarray):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to("cuda")
+
+
+def _run(w: workload.Workload, window: int, horizon: int, bias=None):
+    q, k = _dev(w.q_bits), _dev(w.k_bits)
+    b = None
+    bias = w.bias if bias is None else bias
+    if bias is not None:
+        b = torch.from_numpy(np.ascontiguousarray(bias, dtype=np.float32)).to("cuda")
+    out, lse = kv.kvpop_future_attn_target(q, k, w.scale, window, horizon, key_bias=b)
+    torch.cuda.synchronize()
+    return out.cpu().numpy().astype(np.float64), lse.cpu().numpy().astype(np.float64)
+
+
+def _empty_mask(T: int, window: int) -> np.ndarray:
+    return np.arange(T) + window > T - 1
+
+
+def _check_out(got, ref, window, what=""):
+    T = got.shape[-1]
+    empty = _empty_mask(T, window)
+    assert np.all(got[..., empty] == 0.0), what + ": keys with an empty query range must be exactly 0"
+    g, r = got[..., ~empty], ref[..., ~empty]
+    assert np.all(r > 1e-30), what + ": oracle value below the relative-error floor"
+    rel = np.abs(g - r) / r
+    worst = np.unravel_index(np.argmax(rel), rel.shape) if rel.size else None
+    assert rel.size == 0 or rel.max() <= REL, "%s: max rel err %.3e at %s (gpu %r, oracle %r)" % (
+        what, rel.max(), worst, g[worst], r[worst])
+
+
+def _check_lse(got, ref, what=""):
+    err = np.abs(got - ref)
+    assert err.max() <= LSE_ABS, "%s: lse max abs err %.3e" % (what, err.max())
+
+
+def _cfg(B, Hq, Hkv, T, D, seed, kind="normal", sink=False):
+    return dict(seed=seed, B=B, Hq=Hq, Hkv=Hkv, T=T, D=D, scale=1.0 / math.sqrt(D), kind=kind, sink=sink,
+                bands=[(0, -1)])
+
+
+# ---------------------------------------------------------------------------
+# small and ragged shapes, every band type, against the materialising oracle
+# ---------------------------------------------------------------------------
+
+SHAPES = [
+    # B, Hq, Hkv, T, D
+    (1, 1, 1, 1, 64),
+    (1, 1, 1, 2, 128),
+    (1, 2, 1, 3, 64),
+    (1, 4, 2, 17, 128),
+    (3, 4, 4, 63, 64),
+    (1, 8, 1, 64, 128),
+    (2, 4, 1, 65, 128),
+    (1, 2, 2, 127, 64),
+    (1, 8, 2, 129, 128),
+    (1, 6, 2, 200, 128),
+    (1, 5, 1, 100, 64),
+    (1, 16, 1, 96, 128),
+    (3, 4, 1, 1000, 128),
+    (1, 8, 4, 1000, 64),
+    (1, 4, 1, 1537, 128),
+]
+BANDS = [(0, -1), (1, -1), (1, 1), (1, 1024), (256, -1), (0, 5), (3, 70), (0, 0)]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "B%dHq%dHkv%dT%dD%d" % s)
+def test_shapes_all_bands(shape):
+    B, Hq, Hkv, T, D = shape
+    w = workload.make(_cfg(B, Hq, Hkv, T, D, seed=T * 7 + Hq))
+    lse_ref = oracle.row_lse(w.q_bits, w.k_bits, w.scale)
+    for window, horizon in BANDS:
+        out, lse = _run(w, window, horizon)
+        _check_lse(lse, lse_ref, "shape %s" % (shape,))
+        ref = oracle.future_mass(w.q_bits, w.k_bits, w.scale, None, window, horizon, lse=lse_ref)
+        _check_out(out, ref, window, "shape %s band %s" % (shape, (window, horizon)))
+
+
+@pytest.mark.parametrize("T", [5, 130, 700])
+def test_random_bias_and_masked_keys(T):
+    """Random per-key bias, with every 7th key (from key 1 on) at -inf: masked keys
+    get exactly 0, all others the oracle's value within the relative bar."""
+    w = workload.make(_cfg(1, 4, 2, T, 128, seed=31 + T, kind="rope"))
+    rng = np.random.default_rng(T)
+    bias = rng.standard_normal(T).astype(np.float32) * 2
+    masked = np.zeros(T, bool)
+    masked[1::7] = True
+    bias[masked] = -np.inf
+    lse_ref = oracle.row_lse(w.q_bits, w.k_bits, w.scale, bias)
+    for window, horizon in [(0, -1), (1, 3), (2, -1)]:
+        out, lse = _run(w, window, horizon, bias=bias)
+        _check_lse(lse, lse_ref, "bias")
+        ref = oracle.future_mass(w.q_bits, w.k_bits, w.scale, bias, window, horizon, lse=lse_ref)
+        assert np.all(out[..., masked] == 0.0)
+        keep = ~masked
+        live = keep & ~_empty_mask(T, window)
+        assert np.all(out[..., ~live] == 0.0)
+        rel = np.abs(out[..., live] - ref[..., live]) / ref[..., live]
+        assert rel.max() <= REL, "bias band %s: max rel err %.3e" % ((window, horizon), rel.max())
+
+
+def test_tiny_config():
+    """T=512, one head, D=64, N(0,1) inputs, scale 1/8, full future (window 0)."""
+    w = workload.make("tiny")
+    out, lse = _run(w, 0, -1)
+    ref = oracle.future_mass(w.q_bits, w.k_bits, w.scale)
+    _check_lse(lse, oracle.row_lse(w.q_bits, w.k_bits, w.scale), "tiny")
+    _check_out(out, ref, 0, "tiny")
+    assert out.sum() == pytest.approx(512.0, rel=1e-4)
+
+
+def test_window_beyond_sequence_gives_zeros():
+    w = workload.make(_cfg(1, 2, 1, 100, 128, seed=5))
+    for window, horizon in [(100, -1), (150, 200), (99, 99)]:
+        out, _ = _run(w, window, horizon)
+        if window >= 100:
+            assert np.all(out == 0.0)
+        else:
+            assert np.all(out[..., 1:] == 0.0) and np.all(out[..., 0] > 0)
+
+
+# ---------------------------------------------------------------------------
+# the benchmark workloads
+# ---------------------------------------------------------------------------
+
+def test_qwen3_4b_t4k_sink():
+    """Qwen3-4B shape, T=4096, sink bias on key 0, full future: one query head per KV
+    head (covering every g) against the blocked oracle, all heads by the row sum."""
+    w = workload.make("qwen3_4b_t4k")
+    out, lse = _run(w, 0, -1)
+    np.testing.assert_allclose(out.sum(axis=-1), w.T, rtol=REL)
+    for h in range(w.Hkv):
+        qh = h * w.G + h % w.G
+        q, k = w.q_bits[0, qh], w.k_bits[0, h]
+        lse_ref = oracle.row_lse_blocked(q, k, w.scale, w.bias)
+        _check_lse(lse[0, qh], lse_ref, "4k head %d" % qh)
+        ref = oracle.future_mass_blocked(q, k, w.scale, w.bias, 0, -1, lse=lse_ref)
+        _check_out(out[0, qh], ref, 0, "4k head %d" % qh)
+
+
+def test_qwen3_4b_w1024_band():
+    """Finite horizon W=1024 (j < i <= j + W) with the sink, on a 4096-token cut of
+    the T=16384, B=2 workload (same recipe and seed) against the blocked oracle."""
+    w = workload.make("qwen3_4b_t16k_w1024", T=4096, B=1)
+    out, lse = _run(w, 1, 1024)
+    for qh in (0, 13, 31):
+        q, k = w.q_bits[0, qh], w.k_bits[0, qh // w.G]
+        lse_ref = oracle.row_lse_blocked(q, k, w.scale, w.bias)
+        ref = oracle.future_mass_blocked(q, k, w.scale, w.bias, 1, 1024, lse=lse_ref)
+        _check_out(out[0, qh], ref, 1, "w1024 head %d" % qh)
+
+
+def test_qwen3_4b_w1024_full_size_sampled():
+    """Full T=16384, B=2 W=1024 workload: sampled keys against the oracle's columns."""
+    w = workload.make("qwen3_4b_t16k_w1024")
+    out, lse = _run(w, 1, 1024)
+    rng = np.random.default_rng(0)
+    for b, qh in [(0, 3), (1, 30)]:
+        q, k = w.q_bits[b, qh], w.k_bits[b, qh // w.G]
+        cols = sorted(set(rng.integers(0, w.T, 6).tolist()) | {0, 1, w.T - 1025, w.T - 2, w.T - 1})
+        ref = oracle.future_mass_columns(q, k, w.scale, cols, w.bias, 1, 1024)
+        got = out[b, qh, cols]
+        for c, g, r in zip(cols, got, ref):
+            if c + 1 > w.T - 1:
+                assert g == 0.0
+            else:
+                assert abs(g - r) <= REL * r, (b, qh, c, g, r)
+        rows = rng.integers(0, w.T, 8).tolist()
+        np.testing.assert_allclose(lse[b, qh, rows], oracle.row_lse_rows(q, k, w.scale, rows, w.bias), atol=LSE_ABS,
+                                   rtol=0)
+
+
+def test_qwen3_8b_t32k_full_scale():
+    """Qwen3-8B shape at T=32768, B=4, heavy hitters: the full workload on the GPU,
+    every head by the row sum, sampled LSE rows and the last keys of several heads
+    against the oracle."""
+    w = workload.make("qwen3_8b_t32k")
+    out, lse = _run(w, 0, -1)
+    np.testing.assert_allclose(out.sum(axis=-1), w.T, rtol=REL)
+    rng = np.random.default_rng(1)
+    for b, qh in [(0, 0), (1, 9), (2, 22), (3, 31)]:
+        q, k = w.q_bits[b, qh], w.k_bits[b, qh // w.G]
+        rows = sorted(rng.integers(0, w.T, 6).tolist() + [0, w.T - 1])
+        np.testing.assert_allclose(lse[b, qh, rows], oracle.row_lse_rows(q, k, w.scale, rows), atol=LSE_ABS, rtol=0)
+        cols = list(range(w.T - 40, w.T))
+        ref = oracle.future_mass_columns(q, k, w.scale, cols)
+        _check_out(out[b, qh, cols][None], ref[None], 0, "32k b%d qh%d tail" % (b, qh))
+
+
+def test_qwen3_8b_t32k_one_head_exhaustive():
+    """One (b, query head) of the T=32768 workload, every key, blocked oracle."""
+    b, qh = 2, 6
+    q, k = workload.make_slice("qwen3_8b_t32k", b, qh // 4)
+    q = q[qh % 4]
+    w = workload.make("qwen3_8b_t32k")
+    assert np.array_equal(w.q_bits[b, qh], q)
+    out, lse = _run(w, 0, -1)
+    lse_ref = oracle.row_lse_blocked(q, k, w.scale, block=2048)
+    _check_lse(lse[b, qh], lse_ref, "32k exhaustive")
+    ref = oracle.future_mass_blocked(q, k, w.scale, lse=lse_ref, block=2048)
+    _check_out(out[b, qh], ref, 0, "32k exhaustive")
+
+
+# ---------------------------------------------------------------------------
+# closed forms at full length (T = 131072)
+# ---------------------------------------------------------------------------
+
+def _harmonic(n):
+    # H_n in fp64 by direct summation in reverse (small to large)
+    return np.concatenate([[0.0], np.cumsum(1.0 / np.arange(1, n + 1))])
+
+
+def test_long_q_zero_harmonic():
+    """Q = 0: every row uniform, out_t = H_T - H_t (window 0) and H_{min(T,t+W+1)} -
+    H_{t+1} for the (1, W) band; LSE_d = log(d + 1)."""
+    T = 131072
+    w = workload.make("long_t128k", Hq=4, Hkv=1)
+    w.q_bits[:] = 0
+    H = _harmonic(T + 1)
+    t = np.arange(T)
+    out, lse = _run(w, 0, -1)
+    np.testing.assert_allclose(lse[0, 0], np.log(t + 1.0), atol=LSE_ABS, rtol=0)
+    _check_out(out, np.broadcast_to(H[T] - H[t], out.shape), 0, "harmonic full")
+    out, _ = _run(w, 1, 4096)
+    ref = np.where(t + 1 <= T - 1, H[np.minimum(T, t + 4097)] - H[np.minimum(t + 1, T)], 0.0)
+    _check_out(out, np.broadcast_to(ref, out.shape), 1, "harmonic W=4096")
+
+
+def test_long_constant_query_prefix_form():
+    """All queries of a head equal: p_{d->t} = e^{a_t} / Z_d, so the full-future mass
+    is e^{a_t} * sum_{d >= t} 1 / Z_d -- prefix sums in fp64, real MFMA tiles."""
+    T = 131072
+    w = workload.make("long_t128k", Hq=2, Hkv=1)
+    w.q_bits[:] = w.q_bits[:, :, 1000:1001, :]
+    out, lse = _run(w, 0, -1)
+    for qh in range(2):
+        qv = oracle.bf16_bits_to_f64(w.q_bits[0, qh, 0])
+        kk = oracle.bf16_bits_to_f64(w.k_bits[0, 0])
+        a = w.scale * (kk @ qv)
+        mx = a.max()
+        Z = np.cumsum(np.exp(a - mx))  # scaled by e^{-mx}
+        suffix = np.cumsum((1.0 / Z)[::-1])[::-1]
+        ref = np.exp(a - mx) * suffix
+        np.testing.assert_allclose(lse[0, qh], np.log(Z) + mx, atol=LSE_ABS, rtol=0)
+        _check_out(out[0, qh][None], ref[None], 0, "constant query head %d" % qh)
+
+
+# ---------------------------------------------------------------------------
+# structural properties of the GPU path
+# ---------------------------------------------------------------------------
+
+def test_deterministic_bitwise():
+    w = workload.make("qwen3_4b_t4k")
+    a, la = _run(w, 0, -1)
+    b, lb = _run(w, 0, -1)
+    assert np.array_equal(a, b) and np.array_equal(la, lb)
+
+
+def test_locality_of_finite_horizon():
+    """With band (1, W), out_t depends only on Q rows t+1..t+W and K rows 0..t+W;
+    changing Q and K rows beyond t0 + W leaves keys t <= t0 bitwise unchanged."""
+    T, W, t0 = 2000, 100, 900
+    w = workload.make(_cfg(1, 4, 1, T, 128, seed=77, kind="rope"))
+    a, _ = _run(w, 1, W)
+    w2 = workload.make(_cfg(1, 4, 1, T, 128, seed=78, kind="rope"))
+    w.q_bits[:, :, t0 + W + 1:] = w2.q_bits[:, :, t0 + W + 1:]
+    w.k_bits[:, :, t0 + W + 1:] = w2.k_bits[:, :, t0 + W + 1:]
+    b, _ = _run(w, 1, W)
+    assert np.array_equal(a[..., :t0 + 1], b[..., :t0 + 1])
+    assert not np.array_equal(a, b)
+
+
+def test_external_lse_pass2_only():
+    """kvpop_future_attn_from_lse uses the given normaliser: lse + 0.25 scales every
+    output by exp(-0.25)."""
+    w = workload.make(_cfg(1, 4, 2, 300, 128, seed=9, kind="rope"))
+    q, k = _dev(w.q_bits), _dev(w.k_bits)
+    lse = kv.kvpop_row_lse(q, k, w.scale)
+    o1 = kv.kvpop_future_attn_from_lse(q, k, lse, w.scale, 0, -1)
+    o2 = kv.kvpop_future_attn_from_lse(q, k, lse + 0.25, w.scale, 0, -1)
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(o2.cpu().numpy(), o1.cpu().numpy() * math.exp(-0.25), rtol=1e-5)
+    ref = oracle.future_mass(w.q_bits, w.k_bits, w.scale)
+    _check_out(o1.cpu().numpy().astype(np.float64), ref, 0, "from_lse")
+
+
+def test_gqa_head_permutation():
+    """Permuting the query heads inside a group permutes the outputs (bitwise)."""
+    w = workload.make(_cfg(1, 8, 2, 500, 128, seed=12, kind="rope"))
+    a, _ = _run(w, 0, -1)
+    perm = [2, 0, 3, 1, 5, 4, 7, 6]
+    w.q_bits = np.ascontiguousarray(w.q_bits[:, perm])
+    b, _ = _run(w, 0, -1)
+    assert np.array_equal(b, a[:, perm])
