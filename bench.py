@@ -1,0 +1,213 @@
+"""Benchmark of the future-attention target hot path on one MI355X.
+
+One step = one pass of the whole hot path over one batch of synthetic input:
+pass 1 (row LSE) followed by pass 2 (future mass) for each band of the workload,
+through the C ABI, on torch's current stream, with every input resident in HBM
+before timing starts.
+
+Prints ONE JSON line on stdout. The metric is key-query pairs per second,
+B * Hq * T (T + 1) / 2 / seconds-per-step (every causal pair is scored at least
+once), plus MFMA utilisation = algorithmic MFMA flops (2 * D per scored pair and
+pass; masked tile work not counted) / time / dense bf16 peak.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config NAME] [--skip-cpu]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "key-query pairs/sec and MFMA util (% bf16 peak), Qwen3-8B-shaped layer at T=32k"
+PEAK_BF16_TFLOPS = 2516.6  # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 flop/clk/CU
+KERNEL_SRC = os.path.join(ROOT, "paper_2607_05061_amd", "csrc", "kvpop_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def band_pairs(T: int, window: int, horizon: int) -> int:
+    """Number of (query d, key t) pairs with window <= d - t <= horizon, 0 <= t <= d < T."""
+    hi = T - 1 if horizon < 0 else min(horizon, T - 1)
+    if window > hi:
+        return 0
+    n = hi - window + 1
+    return n * T - (window + hi) * n // 2
+
+
+def kernel_source_hash() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def traffic_for(kernel: str, workload: str):
+    """HBM bytes per launch from committed rocprofv3 counter summaries, or None when
+    absent or taken on a different kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha256") != kernel_source_hash() or t.get("workload") != workload:
+        return None
+    k = t.get("kernels", {}).get(kernel)
+    if not k:
+        return None
+    return k.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, band):
+    """The fp64 oracle, as it stands, on one (batch row, KV head) group of the same
+    workload: its G query heads, row LSE then future mass."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover
+        blas_threads = 1
+    b, h = 0, 0
+    k = w.k_bits[b, h]
+    T = w.T
+    t0 = time.perf_counter()
+    for g in range(w.G):
+        q = w.q_bits[b, h * w.G + g]
+        lse = oracle.row_lse_blocked(q, k, w.scale, w.bias)
+        out = oracle.future_mass_blocked(q, k, w.scale, w.bias, band[0], band[1], lse=lse)
+        assert np.isfinite(out).all()
+    dt = time.perf_counter() - t0
+    pairs = w.G * T * (T + 1) // 2
+    return {
+        "value": pairs / dt,
+        "unit": "pairs/s",
+        "cores": int(blas_threads),
+        "kind": "oracle",
+        "sample": "one (b=0, kv head 0) group of %s: %d query heads x T(T+1)/2 = %d pairs, row LSE then future "
+                  "mass with band %s; fp64 numpy, blocked 1024-row form (BLAS on %d threads, elementwise ops on "
+                  "one); %.1f s" % (w.name, w.G, pairs, tuple(band), blas_threads, dt),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="qwen3_8b_t32k")
+    ap.add_argument("--skip-cpu", action="store_true", help="omit the CPU oracle baseline")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: the future-attention target runs on a single MI355X "
+              "(every (batch, KV head) group is independent; see the sharding design). Use --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2607_05061_amd as kv
+    import workload
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    t_gen = time.perf_counter()
+    w = workload.make(args.config)
+    log("generated %s in %.1f s" % (args.config, time.perf_counter() - t_gen))
+    q = torch.from_numpy(w.q_bits.view(np.int16)).view(torch.bfloat16).to(dev)
+    k = torch.from_numpy(w.k_bits.view(np.int16)).view(torch.bfloat16).to(dev)
+    bias = torch.from_numpy(w.bias).to(dev) if w.bias is not None else None
+    shape = (w.B, w.Hq, w.T)
+    lse = torch.empty(shape, dtype=torch.float32, device=dev)
+    outs = [torch.empty(shape, dtype=torch.float32, device=dev) for _ in w.bands]
+    nb = len(w.bands)
+
+    def step(evs=None):
+        if evs:
+            evs[0].record()
+        kv.kvpop_row_lse(q, k, w.scale, key_bias=bias, lse=lse)
+        if evs:
+            evs[1].record()
+        for i, (win, hor) in enumerate(w.bands):
+            kv.kvpop_future_attn_from_lse(q, k, lse, w.scale, win, hor, key_bias=bias, out=outs[i])
+            if evs:
+                evs[2 + i].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2 + nb)] for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(evs[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    total_ms = evs[0][0].elapsed_time(evs[-1][-1])
+    ms_step = total_ms / args.steps
+    p1_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    p2_ms = [float(np.mean([e[1 + i].elapsed_time(e[2 + i]) for e in evs])) for i in range(nb)]
+
+    pairs_causal = w.B * w.Hq * w.T * (w.T + 1) // 2
+    pairs_p2 = [w.B * w.Hq * band_pairs(w.T, a, b) for a, b in w.bands]
+    flops_p1 = 2.0 * w.D * pairs_causal
+    flops_p2 = [2.0 * w.D * p for p in pairs_p2]
+    value = pairs_causal / (ms_step * 1e-3)
+    util = (flops_p1 + sum(flops_p2)) / (ms_step * 1e-3) / (PEAK_BF16_TFLOPS * 1e12)
+
+    # Dominant kernel: the longest average launch.
+    cands = [("row_lse_kernel", p1_ms, flops_p1)] + [("future_mass_kernel", p2_ms[i], flops_p2[i]) for i in range(nb)]
+    name, dur, fl = max(cands, key=lambda c: c[1])
+    achieved = fl / (dur * 1e-3) / 1e12
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic_for(name, w.name),
+                "kernel": name, "avg_launch_ms": round(dur, 4)}
+
+    # Parity sanity on the live result: full-future masses of a head sum to T.
+    for i, (a, b) in enumerate(w.bands):
+        if a == 0 and b < 0:
+            rs = outs[i].double().sum(dim=-1)
+            err = float((rs / w.T - 1).abs().max())
+            log("row-sum check band %s: max |sum/T - 1| = %.2e" % ((a, b), err))
+            assert err < 2e-3, "row-sum invariant violated"
+
+    cpu = None
+    if not args.skip_cpu:
+        log("timing the CPU oracle on one KV-head group ...")
+        cpu = cpu_baseline(w, w.bands[0])
+
+    res = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "pairs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "T": w.T, "D": w.D,
+                   "bands": [list(b) for b in w.bands], "key_bias": w.bias is not None},
+        "mfma_util": round(util, 4),
+        "pass_ms": {"row_lse": round(p1_ms, 4), "future_mass": [round(x, 4) for x in p2_ms]},
+        "wall_s": round(wall, 3),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()
