@@ -12,13 +12,14 @@
 //
 // Both passes recompute the logits with bf16 MFMA (v_mfma_f32_32x32x16_bf16) and
 // never store the T x T matrix. The reduced index is always put on the MFMA's M
-// (row) axis, so the sum of one output position stays inside one lane across a
+// (row) axis, so the sum for one output position stays inside one lane across a
 // whole sweep: pass 1 computes tiles of K Q^T (keys on rows, queries on columns),
-// pass 2 tiles of Q K^T (queries on rows, keys on columns). The operand that a
+// pass 2 tiles of Q K^T (queries on rows, keys on columns). The operand a
 // workgroup owns for its whole life (Q columns in pass 1, K columns in pass 2)
-// sits in registers; the streamed operand goes through a double-buffered LDS tile
-// that all four waves read, so the query heads of one GQA group share each K tile
-// (pass 1) and all key columns of a workgroup share each Q tile (pass 2).
+// sits in registers as the MFMA B operand; the streamed operand (the A operand)
+// goes through double-buffered LDS tiles that all four waves read, so the query
+// heads of one GQA group share each K tile (pass 1) and all key columns of a
+// workgroup share each Q tile (pass 2).
 //
 // MFMA 32x32x16 lane layout (checked on gfx950): A row m = lane % 32 holds
 // k = 8 * (lane / 32) .. +7; B column n = lane % 32 holds the same k range; the
@@ -26,6 +27,15 @@
 // 8 * (r / 4) + 4 * (lane / 32) + r % 4. The contraction over the head dimension
 // is order-free, so k-step s of a lane uses the 16-byte chunk 2 * s + lane / 32 of
 // the head vector in both operands.
+//
+// Cost model. Per pair and pass the path needs 2 D MFMA flops and, on the vector
+// ALU, one fma, one exp (half rate on gfx950) and one add: at D = 128 the VALU
+// work equals the MFMA time at peak, so the kernels overlap the two explicitly
+// (software-pipelined MFMA chains interleaved with the previous chain's
+// exponentials) and keep every other VALU instruction out of the hot loop:
+// tile loads go straight from global memory to LDS through buffer descriptors,
+// whose range check zero-fills rows past the sequence end instead of clamping
+// addresses.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -38,7 +48,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
@@ -47,6 +57,8 @@ constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kMaxFloor = -1.0e38f;
 // A tile's partial sum above this means the reference maximum was too low.
 constexpr float kOverflow = 18446744073709551616.0f;  // 2^64
+// Buffer descriptor word 3 for raw (untyped) gfx9 buffer access.
+constexpr int kRsrcWord3 = 0x00020000;
 
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
@@ -57,73 +69,83 @@ __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-// A 32-row x D tile of a row-major [T, D] bf16 matrix in LDS. The 16-byte chunk
-// p of row r holds logical chunk p ^ (r % CPR): with 64 lanes reading one logical
-// chunk from 32 consecutive rows, every 16 consecutive rows hit 16 different
-// chunk slots, which spreads a ds_read_b128 over all banks.
+// A 32-row x D bf16 tile in LDS, stored as KS = D / 16 planes of 1 KB. Plane s
+// holds, for MFMA k-step s, the 16-byte chunk 2 s + h of row r at byte
+// 512 h + 16 r. Lane l of a wave therefore finds its A operand of k-step s at
+// byte 1024 s + 16 l: one contiguous, bank-conflict-free 1 KB read per k-step,
+// addressed by a single register plus an immediate offset.
 template <int D>
-struct TileIO {
-  static constexpr int CPR = D / 8;             // 16-byte chunks per row
-  static constexpr int PT = 32 * CPR / 256;     // chunks per thread per tile
-  static_assert(PT >= 1 && (32 * CPR) % 256 == 0, "tile must split evenly over 256 threads");
+struct Tile {
+  static constexpr int KS = D / 16;        // k-steps = planes
+  static constexpr int ELEMS = 32 * D;     // bf16 elements per tile
+  static constexpr int PLANE = 512;        // bf16 elements per plane
 
-  // Global -> registers: rows r0.. of `base` (a [T, D] matrix), clamped to T - 1.
-  static __device__ __forceinline__ void load(u32x4 (&st)[PT], const uint16_t* __restrict__ base, int r0,
-                                              int T, int tid) {
+  // Byte offset, inside a row-major [rows, D] matrix, of the chunk this lane
+  // copies into its plane slot: row lane % 32, chunk half lane / 32.
+  static __device__ __forceinline__ int lane_voffset(int lane) { return (lane & 31) * D * 2 + (lane >> 5) * 16; }
+
+  // Copy planes [s0, s0 + NP) of the tile whose first row is `rows` (a pointer to
+  // `valid` <= 32 rows of a row-major [*, D] matrix) into `lds`; rows >= valid read
+  // as zero. Wave-level: every lane of the calling wave participates.
+  template <int NP>
+  static __device__ __forceinline__ void planes_to_lds(uint16_t* lds, const uint16_t* rows, int valid, int s0,
+                                                       int voff) {
+    const __amdgpu_buffer_rsrc_t r =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(rows), (short)0, valid * D * 2, kRsrcWord3);
 #pragma unroll
-    for (int c = 0; c < PT; ++c) {
-      const int id = tid + 256 * c;
-      const int row = id / CPR;
-      const int p = id % CPR;
-      const int lc = p ^ (row & (CPR - 1));
-      const int src = min(r0 + row, T - 1);
-      st[c] = *reinterpret_cast<const u32x4*>(base + (size_t)src * D + lc * 8);
+    for (int i = 0; i < NP; ++i) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(lds + (s0 + i) * PLANE), 16, voff, (s0 + i) * 32, 0,
+                                               0);
     }
   }
-  // Registers -> LDS: chunk id lands at id * 16 bytes (linear, conflict-free).
-  static __device__ __forceinline__ void store(uint16_t* lds, const u32x4 (&st)[PT], int tid) {
-#pragma unroll
-    for (int c = 0; c < PT; ++c) {
-      const int id = tid + 256 * c;
-      *reinterpret_cast<u32x4*>(lds + id * 8) = st[c];
-    }
-  }
-  // MFMA operand for k-step s of this lane: row l32, logical chunk 2 s + hi.
-  static __device__ __forceinline__ bf16x8 frag(const uint16_t* lds, int l32, int hi, int s) {
-    const int p = (2 * s + hi) ^ (l32 & (CPR - 1));
-    return *reinterpret_cast<const bf16x8*>(lds + (l32 * CPR + p) * 8);
+
+  static __device__ __forceinline__ bf16x8 frag(const uint16_t* lds, int lane, int s) {
+    return *reinterpret_cast<const bf16x8*>(lds + s * PLANE + lane * 8);
   }
 };
+
+// This lane's B operand for all k-steps: row `row` of a row-major [*, D] matrix.
+template <int D>
+__device__ __forceinline__ void load_b_operand(bf16x8 (&f)[D / 16], const uint16_t* row, int hi) {
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s) f[s] = *reinterpret_cast<const bf16x8*>(row + (2 * s + hi) * 8);
+}
 
 // ---------------------------------------------------------------------------
 // Pass 1: row log-normaliser.
 //
 // Workgroup = (batch b, KV head h, head chunk pc of P query heads, query block of
-// BQ = 512 / P positions). Its 4 waves x NQ = 4 column subtiles of 32 (head, query)
-// columns keep their Q rows in registers (the MFMA B operand). Key tiles of 32
-// rows stream through LDS as the A operand, shared by all P heads.
+// BQ = 256 / P positions). Its 4 waves x NQ = 2 column subtiles of 32 (head,
+// query) columns keep their Q rows in registers. One step streams KT = 4 key
+// tiles of 32 rows through LDS (wave w copies tile w), shared by all P heads.
 //
 // Normalisation: every lane keeps, per column subtile, a reference maximum m
-// (log2 units) and sum = sum exp2(x - m) over its 16 rows of each tile. The key
-// tiles that straddle the diagonal are visited first and update (m, sum) exactly,
-// as in online softmax. All later tiles lie strictly below the diagonal; for them
-// the exponentials are taken against the current m without a per-element maximum,
-// and only if a lane's tile sum exceeds 2^64 (a logit more than 64 log2-units
-// above m, or inf) does that lane redo the tile with an exact maximum. The result
-// is the same LSE; the common path costs one fma, one exp and one add per pair.
+// (log2 units) and sum = sum exp2(x - m) over its 16 rows of each tile. Key tiles
+// are visited diagonal-first: the tiles that straddle the diagonal (and any step
+// that shares them) update (m, sum) exactly, as in online softmax. Every later
+// step lies strictly below the diagonal and takes the exponentials against the
+// current m with no per-element maximum; a lane whose tile sum exceeds 2^64 (a
+// logit more than 64 log2-units above m, or inf) flags the step, which is then
+// redone exactly from the LDS tiles. The result is the same LSE; the common path
+// costs one fma, one exp and one add per pair.
 // ---------------------------------------------------------------------------
-template <int D, bool HAS_BIAS>
+template <int D, int P, bool HAS_BIAS>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2))) void
 row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const float* __restrict__ bias,
-               float* __restrict__ lse, int B, int Hq, int Hkv, int T, float c, float inv_scale, int P,
-               int nqb) {
-  constexpr int NQ = 4;
-  constexpr int KS = D / 16;
-  using IO = TileIO<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t sk[2][32 * D];
-  __shared__ __attribute__((aligned(16))) float sb[2][32];
+               float* __restrict__ lse, int B, int Hq, int Hkv, int T, float c, float inv_scale, int nqb) {
+  constexpr int NQ = 2;
+  constexpr int KT = 4;
+  using TL = Tile<D>;
+  constexpr int KS = TL::KS;
+  constexpr int SPH = 8 / P;  // column subtiles per head
+  constexpr int BQ = 32 * SPH;
+  __shared__ __attribute__((aligned(16))) uint16_t sk0[KT * TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) uint16_t sk1[KT * TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) float sb0[KT * 32];
+  __shared__ __attribute__((aligned(16))) float sb1[KT * 32];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, hi = lane >> 5, l32 = lane & 31;
+  const int tid = threadIdx.x, lane = tid & 63, hi = lane >> 5, l32 = lane & 31;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, uniform per wave
   const int G = Hq / Hkv;
   const int npc = G / P;
   const int per = B * Hkv * npc;
@@ -134,49 +156,46 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
   rest -= b * Hkv * npc;
   const int h = rest / npc;
   const int pc = rest - h * npc;
-  const int SPH = 16 / P;  // column subtiles per head in this block
-  const int BQ = 32 * SPH;
   const int i0 = qb * BQ;
 
   int qs[NQ], qh[NQ];
+  bf16x8 qf[NQ][KS];  // this lane's query rows (B operand), resident for the whole sweep
 #pragma unroll
   for (int n = 0; n < NQ; ++n) {
     const int u = w * NQ + n;
     qs[n] = i0 + 32 * (u % SPH);
     qh[n] = h * G + pc * P + u / SPH;
-  }
-
-  // This lane's query rows (B operand), resident for the whole sweep.
-  bf16x8 qf[NQ][KS];
-#pragma unroll
-  for (int n = 0; n < NQ; ++n) {
     const int q = min(qs[n] + l32, T - 1);
-    const uint16_t* src = Q + ((size_t)(b * Hq + qh[n]) * T + q) * D;
-#pragma unroll
-    for (int s = 0; s < KS; ++s) qf[n][s] = *reinterpret_cast<const bf16x8*>(src + (2 * s + hi) * 8);
+    load_b_operand<D>(qf[n], Q + ((size_t)(b * Hq + qh[n]) * T + q) * D, hi);
   }
 
   const uint16_t* Kbh = K + (size_t)(b * Hkv + h) * T * D;
   const int kend = min(T, i0 + BQ);
-  const int nkt = (kend + 31) / 32;
-  const int nfull = i0 / 32;  // tiles with every key below the block's first query
+  const int nkt = (kend + 31) / 32;  // key tiles 0 .. nkt - 1
+  const int nfull = i0 / 32;         // tiles with every key below the block's first query
   const int ndiag = nkt - nfull;
+  const int nsteps = (nkt + KT - 1) / KT;
+  const int diag_steps = (ndiag + KT - 1) / KT;
+  // Visiting order: diagonal tiles from the top down, then the rest from key 0 up
+  // (so the workgroups of one KV head stream the same K tiles at the same time).
+  auto tile_of = [&](int idx) __attribute__((always_inline)) { return idx < ndiag ? nkt - 1 - idx : idx - ndiag; };
 
-  auto tile_of = [&](int s) { return s < ndiag ? nkt - 1 - s : s - ndiag; };
-
-  u32x4 st[IO::PT];
+  const int voff = TL::lane_voffset(lane);
   float stb = 0.f;
-  auto fetch = [&](int s) {
-    const int t0 = tile_of(s) * 32;
-    IO::load(st, Kbh, t0, T, tid);
-    if (HAS_BIAS && tid < 32) {
-      const int t = t0 + tid;
+  auto issue = [&](int s, uint16_t* sk) __attribute__((always_inline)) {
+    const int idx = s * KT + w;
+    if (idx < nkt) {
+      const int t0 = tile_of(idx) * 32;
+      TL::template planes_to_lds<KS>(sk + w * TL::ELEMS, Kbh + (size_t)t0 * D, min(32, T - t0), 0, voff);
+    }
+    if (HAS_BIAS && tid < KT * 32) {
+      const int idx2 = s * KT + (tid >> 5);
+      const int t = idx2 < nkt ? tile_of(idx2) * 32 + (tid & 31) : T;
       stb = t < T ? bias[t] * inv_scale : 0.f;
     }
   };
-  auto commit = [&](int buf) {
-    IO::store(sk[buf], st, tid);
-    if (HAS_BIAS && tid < 32) sb[buf][tid] = stb;
+  auto commit = [&](float* sb) __attribute__((always_inline)) {
+    if (HAS_BIAS && tid < KT * 32) sb[tid] = stb;
   };
 
   float m[NQ], sum[NQ];
@@ -186,84 +205,140 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
     sum[n] = 0.f;
   }
 
-  fetch(0);
-  commit(0);
-  __syncthreads();
-
-  for (int s = 0; s < nkt; ++s) {
-    const int cur = s & 1;
-    if (s + 1 < nkt) fetch(s + 1);
-    const int t0 = tile_of(s) * 32;
-
-    f32x16 acc[NQ];
+  // Accumulator start value: 0, or bias_t / scale on the key rows, so that
+  // acc * c = (scale <q, k_t> + bias_t) * log2(e).
+  auto acc_init = [&](const float* sb, int u) __attribute__((always_inline)) {
+    f32x16 a = f32x16{};
     if (HAS_BIAS) {
-      // Bias enters through the accumulator: C = bias_t / scale, so acc * c is
-      // (scale <q, k_t> + bias_t) * log2(e).
-      f32x16 ci;
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
-        const f32x4 v = *reinterpret_cast<const f32x4*>(&sb[cur][8 * g4 + 4 * hi]);
-        ci[4 * g4 + 0] = v[0];
-        ci[4 * g4 + 1] = v[1];
-        ci[4 * g4 + 2] = v[2];
-        ci[4 * g4 + 3] = v[3];
+        const f32x4 v = *reinterpret_cast<const f32x4*>(&sb[u * 32 + 8 * g4 + 4 * hi]);
+        a[4 * g4 + 0] = v[0];
+        a[4 * g4 + 1] = v[1];
+        a[4 * g4 + 2] = v[2];
+        a[4 * g4 + 3] = v[3];
       }
+    }
+    return a;
+  };
+  auto chain = [&](const uint16_t* sk, const float* sb, int u, int n) __attribute__((always_inline)) {
+    f32x16 acc = acc_init(sb, u);
 #pragma unroll
-      for (int n = 0; n < NQ; ++n) acc[n] = ci;
+    for (int ks = 0; ks < KS; ++ks) acc = mfma32(TL::frag(sk + u * TL::ELEMS, lane, ks), qf[n][ks], acc);
+    return acc;
+  };
+
+  // Exact online update of (m, sum) with the admissible entries of one tile.
+  auto exact_update = [&](const f32x16& acc, int t0, int n, bool partial) __attribute__((always_inline)) {
+    const int q = qs[n] + l32;
+    float v[16];
+    float tmax = kMaxFloor;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      v[r] = acc[r] * c;
+      if (partial && t0 + acc_row(r, hi) > q) v[r] = -__builtin_inff();
+      tmax = fmaxf(tmax, v[r]);
+    }
+    const float mn = fmaxf(m[n], tmax);
+    float e = 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) e += exp2_fast(v[r] - mn);
+    sum[n] = sum[n] * exp2_fast(m[n] - mn) + e;
+    m[n] = mn;
+  };
+  // The exact path over every valid tile of a step.
+  auto exact_step = [&](int s, const uint16_t* sk, const float* sb) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < KT; ++u) {
+      const int idx = s * KT + u;
+      if (idx < nkt) {
+        const int t0 = tile_of(idx) * 32;
+#pragma unroll
+        for (int n = 0; n < NQ; ++n) {
+          if (t0 <= qs[n] + 31) {
+            const f32x16 acc = chain(sk, sb, u, n);
+            exact_update(acc, t0, n, t0 + 31 > qs[n]);
+          }
+        }
+      }
+    }
+  };
+
+  // Fast path: units v = (tile u, subtile n) as a software pipeline with a fixed
+  // issue order (scheduling barriers keep the compiler from regrouping it): k-step
+  // ks of unit v issues its MFMA, refills the A fragment register it consumed with
+  // the operand of unit v + 1 (used KS MFMAs later, hiding the LDS latency), and
+  // does the exp/accumulate work of 16 / KS elements of unit v - 1.
+  auto fast_step = [&](const uint16_t* sk, const float* sb) __attribute__((always_inline)) {
+    constexpr int U = KT * NQ;
+    constexpr int EPK = 16 / KS;
+    float nm[NQ];
+#pragma unroll
+    for (int n = 0; n < NQ; ++n) nm[n] = -m[n];
+    bool ovf = false;
+    bf16x8 fr[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) fr[ks] = TL::frag(sk, lane, ks);
+    f32x16 acc_prev;
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int v = 0; v <= U; ++v) {
+      const int u = v / NQ, n = v % NQ, un = (v + 1) / NQ, np = (v + NQ - 1) % NQ;
+      f32x16 acc = v < U ? acc_init(sb, u) : f32x16{};
+      float ts0 = 0.f, ts1 = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        if (v < U) {
+          acc = mfma32(fr[ks], qf[n][ks], acc);
+          if (v + 1 < U) fr[ks] = TL::frag(sk + un * TL::ELEMS, lane, ks);
+        }
+        if (v > 0) {
+#pragma unroll
+          for (int e = 0; e < EPK; ++e) {
+            const int r = ks * EPK + e;
+            const float x = exp2_fast(__builtin_fmaf(acc_prev[r], c, nm[np]));
+            if (e & 1) ts1 += x; else ts0 += x;
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (v > 0) {
+        const float ts = ts0 + ts1;
+        sum[np] += ts;
+        ovf |= !(ts <= kOverflow);
+      }
+      acc_prev = acc;
+    }
+    return ovf;
+  };
+
+  auto step = [&](int s, const uint16_t* sk, const float* sb, uint16_t* nsk, float* nsb) __attribute__((always_inline)) {
+    const bool more = s + 1 < nsteps;
+    if (more) issue(s + 1, nsk);
+    if (s >= diag_steps && (s + 1) * KT <= nkt) {
+      float saved[NQ];
+#pragma unroll
+      for (int n = 0; n < NQ; ++n) saved[n] = sum[n];
+      const bool ovf = fast_step(sk, sb);
+      if (__builtin_amdgcn_ballot_w64(ovf) != 0) {
+        // Some lane met a logit far above its reference maximum: redo exactly.
+#pragma unroll
+        for (int n = 0; n < NQ; ++n) sum[n] = saved[n];
+        exact_step(s, sk, sb);
+      }
     } else {
-#pragma unroll
-      for (int n = 0; n < NQ; ++n) acc[n] = f32x16{};
+      exact_step(s, sk, sb);
     }
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const bf16x8 a = IO::frag(sk[cur], l32, hi, ks);
-#pragma unroll
-      for (int n = 0; n < NQ; ++n) acc[n] = mfma32(a, qf[n][ks], acc[n]);
-    }
-
-#pragma unroll
-    for (int n = 0; n < NQ; ++n) {
-      if (t0 + 31 <= qs[n]) {
-        // Strictly below the diagonal for every column of the subtile.
-        const float nm = -m[n];
-        float ts = 0.f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) ts += exp2_fast(__builtin_fmaf(acc[n][r], c, nm));
-        if (!(ts <= kOverflow)) {
-          float tmax = kMaxFloor;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, acc[n][r] * c);
-          const float mn = fmaxf(m[n], tmax);
-          float e = 0.f;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) e += exp2_fast(__builtin_fmaf(acc[n][r], c, -mn));
-          sum[n] = sum[n] * exp2_fast(m[n] - mn) + e;
-          m[n] = mn;
-        } else {
-          sum[n] += ts;
-        }
-      } else if (t0 <= qs[n] + 31) {
-        // Straddles the diagonal: key t is admissible for query q iff t <= q.
-        const int q = qs[n] + l32;
-        float v[16];
-        float tmax = kMaxFloor;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int t = t0 + acc_row(r, hi);
-          v[r] = t <= q ? acc[n][r] * c : -__builtin_inff();
-          tmax = fmaxf(tmax, v[r]);
-        }
-        const float mn = fmaxf(m[n], tmax);
-        float e = 0.f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) e += exp2_fast(v[r] - mn);
-        sum[n] = sum[n] * exp2_fast(m[n] - mn) + e;
-        m[n] = mn;
-      }
-    }
-
-    if (s + 1 < nkt) commit(cur ^ 1);
+    if (more) commit(nsb);
     __syncthreads();
+  };
+
+  issue(0, sk0);
+  commit(sb0);
+  __syncthreads();
+  for (int s = 0; s < nsteps; s += 2) {
+    step(s, sk0, sb0, sk1, sb1);
+    if (s + 1 < nsteps) step(s + 1, sk1, sb1, sk0, sb0);
   }
 
   // Merge the two half-wave partials of each column and write LSE (natural log).
@@ -281,33 +356,42 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
 // ---------------------------------------------------------------------------
 // Pass 2: future mass per key.
 //
-// Workgroup = (batch b, KV head h, key block of BK = 4 * NK * 32 keys); wave w owns
-// NK column subtiles of 32 keys whose K rows stay in registers (the MFMA B
-// operand). For each query head of the group in turn, the workgroup sweeps the
-// query tiles of 32 rows that can see its keys; each Q tile and its 32 LSE values
-// are staged once in LDS and read by all four waves. Every lane accumulates, for
-// its key column, exp2(acc * c - LSE_d * log2 e) over its 16 query rows of each
-// tile into a per-tile sum and then into a running column sum (a two-level sum
-// keeps the fp32 error near (16 + number of tiles) ulp). After a head's sweep the
-// two half-wave sums of each column are added and written out: each workgroup owns
-// its output columns, so no atomics are needed and results are deterministic.
+// Workgroup = (batch b, KV head h, key block of BK = 4 * NS * 32 keys); wave w owns
+// NS column subtiles of 32 keys whose K rows stay in registers. The workgroup
+// sweeps the query tiles of 32 rows that can see its keys from the last one down;
+// one step stages the tiles of GC query heads of the group in LDS together with
+// their LSE values, and every wave reads them all. Descending order keeps the key
+// blocks of one KV head -- which all end at the last query row -- on the same tile
+// at the same time, so they share it through L2.
+//
+// Every lane accumulates, for its key column, exp2(acc * c - LSE_d * log2 e) over
+// its 16 query rows of each tile into a per-tile sum and then into a running
+// column sum (a two-level sum keeps the fp32 error near (16 + tiles) ulp). At the
+// end the two half-wave sums of each column are added and written: each workgroup
+// owns its output columns, so no atomics are needed and results are deterministic.
 //
 // Query rows beyond T get LSE = +inf in LDS, which zeroes their terms. A per-key
-// bias is factored out of the sum, out_t = exp(bias_t) * sum_d exp(...).
+// bias is factored out of the sum, out_t = exp(bias_t) * sum_d exp(...). Query
+// heads are processed GC at a time; G / GC chunks each repeat the sweep.
 // ---------------------------------------------------------------------------
-template <int D, int NK, bool HAS_BIAS>
+template <int D, int NS, int GC, bool HAS_BIAS>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2))) void
 future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const float* __restrict__ bias,
                    const float* __restrict__ lse, float* __restrict__ out, int B, int Hq, int Hkv, int T, float c,
                    int window, int hz) {
-  constexpr int KS = D / 16;
-  constexpr int WK = NK * 32;  // keys per wave
+  using TL = Tile<D>;
+  constexpr int KS = TL::KS;
+  constexpr int WK = NS * 32;  // keys per wave
   constexpr int BK = 4 * WK;   // keys per workgroup
-  using IO = TileIO<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t sq[2][32 * D];
-  __shared__ __attribute__((aligned(16))) float sl[2][32];
+  constexpr int PPW = GC * KS / 4;  // LDS planes each wave copies per step
+  static_assert(PPW >= 1 && KS % PPW == 0, "plane split");
+  __shared__ __attribute__((aligned(16))) uint16_t sq0[GC * TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) uint16_t sq1[GC * TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) float sl0[GC * 32];
+  __shared__ __attribute__((aligned(16))) float sl1[GC * 32];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, hi = lane >> 5, l32 = lane & 31;
+  const int tid = threadIdx.x, lane = tid & 63, hi = lane >> 5, l32 = lane & 31;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, uniform per wave
   const int G = Hq / Hkv;
   const int nbh = B * Hkv;
   const int kb = blockIdx.x / nbh;  // key block 0 (most query rows) first
@@ -320,15 +404,15 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
   // Query rows that can reach any key of the block: [j0 + window, j0 + BK - 1 + hz] within [0, T).
   const long long r_lo = (long long)j0 + window;
   const long long r_hi = min((long long)T - 1, (long long)j0 + BK - 1 + hz);
-  int qt0 = 0, nqt = 0;
+  int qt_hi = 0, nqt = 0;
   if (r_lo <= r_hi) {
-    qt0 = (int)(r_lo / 32);
-    nqt = (int)(r_hi / 32) - qt0 + 1;
+    qt_hi = (int)(r_hi / 32);
+    nqt = qt_hi - (int)(r_lo / 32) + 1;
   }
 
-  float fac[NK];
+  float fac[NS];
 #pragma unroll
-  for (int n = 0; n < NK; ++n) {
+  for (int n = 0; n < NS; ++n) {
     fac[n] = 1.f;
     if (HAS_BIAS) {
       const int j = min(jw + 32 * n + l32, T - 1);
@@ -341,7 +425,7 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     // Every key of the block has an empty query range.
     for (int g = 0; g < G; ++g) {
 #pragma unroll
-      for (int n = 0; n < NK; ++n) {
+      for (int n = 0; n < NS; ++n) {
         const int j = jw + 32 * n + l32;
         if (hi == 0 && j < T) out[(size_t)(b * Hq + h * G + g) * T + j] = 0.f;
       }
@@ -349,164 +433,229 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     return;
   }
 
-  // This lane's key rows (B operand), resident for the whole sweep.
-  bf16x8 kf[NK][KS];
+  bf16x8 kf[NS][KS];  // this lane's key rows (B operand), resident for the whole sweep
   const uint16_t* Kbh = K + (size_t)bh * T * D;
 #pragma unroll
-  for (int n = 0; n < NK; ++n) {
-    const int j = min(jw + 32 * n + l32, T - 1);
-#pragma unroll
-    for (int s = 0; s < KS; ++s) kf[n][s] = *reinterpret_cast<const bf16x8*>(Kbh + (size_t)j * D + (2 * s + hi) * 8);
-  }
+  for (int n = 0; n < NS; ++n) load_b_operand<D>(kf[n], Kbh + (size_t)min(jw + 32 * n + l32, T - 1) * D, hi);
 
-  const int nsteps = nqt * G;
-  u32x4 st[IO::PT];
-  float stl = 0.f;
-  auto fetch = [&](int s) {
-    const int g = s / nqt;
-    const int i0 = (qt0 + s - g * nqt) * 32;
-    const size_t head = (size_t)(b * Hq + h * G + g);
-    IO::load(st, Q + head * T * D, i0, T, tid);
-    if (tid < 32) {
-      const int i = i0 + tid;
-      stl = i < T ? -lse[head * T + i] * kLog2e : -__builtin_inff();
-    }
-  };
-  auto commit = [&](int buf) {
-    IO::store(sq[buf], st, tid);
-    if (tid < 32) sl[buf][tid] = stl;
-  };
+  const int voff = TL::lane_voffset(lane);
+  const int pg = (w * PPW) / KS;          // the head tile this wave copies
+  const int ps0 = (w * PPW) - pg * KS;    // its first plane
 
-  fetch(0);
-  commit(0);
-  __syncthreads();
-
-  float colsum[NK];
-#pragma unroll
-  for (int n = 0; n < NK; ++n) colsum[n] = 0.f;
-  int g = 0, qi = 0;  // head and tile index of step s
-
-  for (int s = 0; s < nsteps; ++s) {
-    const int cur = s & 1;
-    if (s + 1 < nsteps) fetch(s + 1);
-    const int i0 = (qt0 + qi) * 32;
-
-    // Differences d = i - j over this wave's keys and the tile's rows.
-    const int dmin = i0 - (jw + WK - 1);
-    const int dmax = i0 + 31 - jw;
-    const bool none = dmax < window || dmin > hz;
-    if (!none) {
-      f32x16 acc[NK];
-#pragma unroll
-      for (int n = 0; n < NK; ++n) acc[n] = f32x16{};
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8 a = IO::frag(sq[cur], l32, hi, ks);
-#pragma unroll
-        for (int n = 0; n < NK; ++n) acc[n] = mfma32(a, kf[n][ks], acc[n]);
+  for (int gh0 = h * G; gh0 < (h + 1) * G; gh0 += GC) {
+    const size_t head0 = (size_t)(b * Hq + gh0);
+    float stl = 0.f;
+    // Start the loads of step s: Q tiles straight into LDS, raw LSE into a register.
+    auto issue = [&](int s, uint16_t* sq) __attribute__((always_inline)) {
+      const int i0 = (qt_hi - s) * 32;
+      TL::template planes_to_lds<PPW>(sq + pg * TL::ELEMS, Q + ((head0 + pg) * T + i0) * D, min(32, T - i0), ps0,
+                                      voff);
+      if (tid < GC * 32) {
+        const int i = i0 + (tid & 31);
+        stl = i < T ? lse[(head0 + (tid >> 5)) * T + i] : __builtin_inff();
       }
-      float nl[16];
+    };
+    auto commit = [&](float* sl) __attribute__((always_inline)) {
+      if (tid < GC * 32) sl[tid] = -stl * kLog2e;
+    };
+
+    float colsum[GC][NS];
+#pragma unroll
+    for (int g = 0; g < GC; ++g)
+#pragma unroll
+      for (int n = 0; n < NS; ++n) colsum[g][n] = 0.f;
+
+    auto read_nl = [&](const float* sl, int g, float (&nl)[16]) {
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
-        const f32x4 v = *reinterpret_cast<const f32x4*>(&sl[cur][8 * g4 + 4 * hi]);
+        const f32x4 v = *reinterpret_cast<const f32x4*>(&sl[g * 32 + 8 * g4 + 4 * hi]);
         nl[4 * g4 + 0] = v[0];
         nl[4 * g4 + 1] = v[1];
         nl[4 * g4 + 2] = v[2];
         nl[4 * g4 + 3] = v[3];
       }
-      const bool full = dmin >= window && dmax <= hz;
-      if (full) {
+    };
+    auto accumulate = [&](const f32x16& acc, const float (&nl)[16], float& cs) {
+      float ts = 0.f;
 #pragma unroll
-        for (int n = 0; n < NK; ++n) {
-          float ts = 0.f;
+      for (int r = 0; r < 16; ++r) ts += exp2_fast(__builtin_fmaf(acc[r], c, nl[r]));
+      cs += ts;
+    };
+
+    // Fully admissible step: U = GC * NS units (head g, key subtile n) of KS MFMAs
+    // each, as a software pipeline whose issue order is fixed group by group (the
+    // scheduling barriers stop the compiler from regrouping it): k-step ks of unit
+    // u issues its MFMA, refills the A fragment register it just consumed with the
+    // operand of unit u + 1 (used KS MFMAs later, so the LDS latency is hidden),
+    // and does the exp/accumulate work of 16 / KS elements of unit u - 1, whose
+    // accumulators completed long before.
+    auto full_step = [&](const uint16_t* sq, const float* sl) __attribute__((always_inline)) {
+      constexpr int U = GC * NS;
+      constexpr int EPK = 16 / KS;  // elements of the previous unit per k-step
+      bf16x8 fr[KS];
+      float nl[2][16];
+      f32x16 acc_prev;
 #pragma unroll
-          for (int r = 0; r < 16; ++r) ts += exp2_fast(__builtin_fmaf(acc[n][r], c, nl[r]));
-          colsum[n] += ts;
+      for (int ks = 0; ks < KS; ++ks) fr[ks] = TL::frag(sq, lane, ks);
+      read_nl(sl, 0, nl[0]);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int u = 0; u <= U; ++u) {
+        const int g = u / NS, n = u % NS, gn = (u + 1) / NS;
+        const int gp = (u - 1) / NS, np = (u - 1) % NS;
+        if (u > 0 && u < U && n == 0) read_nl(sl, g, nl[g & 1]);
+        f32x16 acc = f32x16{};
+        float ts0 = 0.f, ts1 = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          if (u < U) {
+            acc = mfma32(fr[ks], kf[n % NS][ks], acc);
+            if (u + 1 < U) fr[ks] = TL::frag(sq + gn * TL::ELEMS, lane, ks);
+          }
+          if (u > 0) {
+#pragma unroll
+            for (int e = 0; e < EPK; ++e) {
+              const int r = ks * EPK + e;
+              const float x = exp2_fast(__builtin_fmaf(acc_prev[r], c, nl[gp & 1][r]));
+              if (e & 1) ts1 += x; else ts0 += x;
+            }
+          }
+          __builtin_amdgcn_sched_barrier(0);
         }
-      } else {
+        if (u > 0) colsum[gp][np] += ts0 + ts1;
+        acc_prev = acc;
+      }
+    };
+
+    // Tile on a band edge: mask each pair by window <= i - j <= hz.
+    auto edge_step = [&](const uint16_t* sq, const float* sl, int i0) __attribute__((always_inline)) {
 #pragma unroll
-        for (int n = 0; n < NK; ++n) {
+      for (int g = 0; g < GC; ++g) {
+        float nl[16];
+        read_nl(sl, g, nl);
+#pragma unroll
+        for (int n = 0; n < NS; ++n) {
+          f32x16 acc = f32x16{};
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) acc = mfma32(TL::frag(sq + g * TL::ELEMS, lane, ks), kf[n][ks], acc);
           const int base = i0 + 4 * hi - (jw + 32 * n + l32);
           float ts = 0.f;
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int d = base + 8 * (r >> 2) + (r & 3);
-            const float e = exp2_fast(__builtin_fmaf(acc[n][r], c, nl[r]));
+            const float e = exp2_fast(__builtin_fmaf(acc[r], c, nl[r]));
             ts += (d >= window && d <= hz) ? e : 0.f;
           }
-          colsum[n] += ts;
+          colsum[g][n] += ts;
         }
       }
+    };
+
+    auto step = [&](int s, const uint16_t* sq, const float* sl, uint16_t* nsq, float* nsl) __attribute__((always_inline)) {
+      const bool more = s + 1 < nqt;
+      if (more) issue(s + 1, nsq);
+      const int i0 = (qt_hi - s) * 32;
+      // Differences d = i - j over this wave's keys and the tile's rows.
+      const int dmin = i0 - (jw + WK - 1);
+      const int dmax = i0 + 31 - jw;
+      if (dmin >= window && dmax <= hz) {
+        full_step(sq, sl);
+      } else if (!(dmax < window || dmin > hz)) {
+        edge_step(sq, sl, i0);
+      }
+      if (more) commit(nsl);
+      __syncthreads();
+    };
+
+    issue(0, sq0);
+    commit(sl0);
+    __syncthreads();
+    for (int s = 0; s < nqt; s += 2) {
+      step(s, sq0, sl0, sq1, sl1);
+      if (s + 1 < nqt) step(s + 1, sq1, sl1, sq0, sl0);
     }
 
-    if (s + 1 < nsteps) commit(cur ^ 1);
-    __syncthreads();
-
-    if (++qi == nqt) {
-      // End of head g's sweep: combine the half-wave sums and write its columns.
+    // Combine the half-wave sums and write this chunk's columns.
 #pragma unroll
-      for (int n = 0; n < NK; ++n) {
-        const float v = colsum[n] + __shfl_xor(colsum[n], 32);
+    for (int g = 0; g < GC; ++g) {
+#pragma unroll
+      for (int n = 0; n < NS; ++n) {
+        const float v = colsum[g][n] + __shfl_xor(colsum[g][n], 32);
         const int j = jw + 32 * n + l32;
-        if (hi == 0 && j < T) out[(size_t)(b * Hq + h * G + g) * T + j] = HAS_BIAS ? v * fac[n] : v;
-        colsum[n] = 0.f;
+        if (hi == 0 && j < T) out[(head0 + g) * T + j] = HAS_BIAS ? v * fac[n] : v;
       }
-      qi = 0;
-      ++g;
     }
   }
 }
 
-template <int D, bool HB>
-int launch_p1(const Launch& L, int P) {
+template <int D, int P, bool HB>
+int launch_p1(const Launch& L) {
+  constexpr int BQ = 256 / P;
   const int G = L.Hq / L.Hkv;
-  const int BQ = 512 / P;
   const int nqb = (L.T + BQ - 1) / BQ;
   const long long grid = (long long)nqb * L.B * L.Hkv * (G / P);
   const float c = L.scale * kLog2e;
-  hipLaunchKernelGGL((row_lse_kernel<D, HB>), dim3((unsigned)grid), dim3(256), 0, (hipStream_t)L.stream,
+  hipLaunchKernelGGL((row_lse_kernel<D, P, HB>), dim3((unsigned)grid), dim3(256), 0, (hipStream_t)L.stream,
                      reinterpret_cast<const uint16_t*>(L.q), reinterpret_cast<const uint16_t*>(L.k), L.bias, L.out,
-                     L.B, L.Hq, L.Hkv, L.T, c, 1.0f / L.scale, P, nqb);
+                     L.B, L.Hq, L.Hkv, L.T, c, 1.0f / L.scale, nqb);
   return (int)hipGetLastError();
 }
 
-template <int D, int NK, bool HB>
+template <int D, int P>
+int launch_p1_b(const Launch& L) {
+  return L.bias ? launch_p1<D, P, true>(L) : launch_p1<D, P, false>(L);
+}
+
+template <int D>
+int launch_p1_d(const Launch& L) {
+  // Query heads per workgroup: the largest power of two dividing G, at most 8.
+  const int G = L.Hq / L.Hkv;
+  if (G % 8 == 0) return launch_p1_b<D, 8>(L);
+  if (G % 4 == 0) return launch_p1_b<D, 4>(L);
+  if (G % 2 == 0) return launch_p1_b<D, 2>(L);
+  return launch_p1_b<D, 1>(L);
+}
+
+template <int D, int NS, int GC, bool HB>
 int launch_p2(const Launch& L) {
-  constexpr int BK = 4 * NK * 32;
+  constexpr int BK = 4 * NS * 32;
   const int nkb = (L.T + BK - 1) / BK;
   const long long grid = (long long)nkb * L.B * L.Hkv;
   const float c = L.scale * kLog2e;
   const int hz = L.horizon < 0 ? L.T : L.horizon;
-  hipLaunchKernelGGL((future_mass_kernel<D, NK, HB>), dim3((unsigned)grid), dim3(256), 0, (hipStream_t)L.stream,
+  hipLaunchKernelGGL((future_mass_kernel<D, NS, GC, HB>), dim3((unsigned)grid), dim3(256), 0, (hipStream_t)L.stream,
                      reinterpret_cast<const uint16_t*>(L.q), reinterpret_cast<const uint16_t*>(L.k), L.bias, L.lse,
                      L.out, L.B, L.Hq, L.Hkv, L.T, c, L.window, hz);
   return (int)hipGetLastError();
 }
 
-template <int D, int NK>
-int launch_p2_nk(const Launch& L) {
-  return L.bias ? launch_p2<D, NK, true>(L) : launch_p2<D, NK, false>(L);
+template <int D, int NS, int GC>
+int launch_p2_b(const Launch& L) {
+  return L.bias ? launch_p2<D, NS, GC, true>(L) : launch_p2<D, NS, GC, false>(L);
+}
+
+template <int D, int NS>
+int launch_p2_gc(const Launch& L) {
+  // Query heads per step: the largest of 4, 2, 1 that divides G.
+  const int G = L.Hq / L.Hkv;
+  if (G % 4 == 0) return launch_p2_b<D, NS, 4>(L);
+  if (G % 2 == 0) return launch_p2_b<D, NS, 2>(L);
+  return launch_p2_b<D, NS, 1>(L);
 }
 
 template <int D>
 int launch_p2_d(const Launch& L) {
-  // Largest key block that still gives every CU about two workgroups.
-  const long long bh = (long long)L.B * L.Hkv;
-  const long long wg4 = bh * ((L.T + 511) / 512);
-  const long long wg2 = bh * ((L.T + 255) / 256);
-  if (wg4 >= 512) return launch_p2_nk<D, 4>(L);
-  if (wg2 >= 512) return launch_p2_nk<D, 2>(L);
-  return launch_p2_nk<D, 1>(L);
+  // Two key subtiles per wave unless that leaves fewer than ~2 workgroups per CU.
+  const long long wg2 = (long long)L.B * L.Hkv * ((L.T + 255) / 256);
+  if (wg2 >= 512) return launch_p2_gc<D, 2>(L);
+  return launch_p2_gc<D, 1>(L);
 }
 
 }  // namespace
 
 int launch_row_lse(const Launch& L) {
-  const int G = L.Hq / L.Hkv;
-  int P = G & -G;  // largest power of two dividing G, at most 16
-  if (P > 16) P = 16;
-  if (L.D == 64) return L.bias ? launch_p1<64, true>(L, P) : launch_p1<64, false>(L, P);
-  return L.bias ? launch_p1<128, true>(L, P) : launch_p1<128, false>(L, P);
+  if (L.D == 64) return launch_p1_d<64>(L);
+  return launch_p1_d<128>(L);
 }
 
 int launch_future_mass(const Launch& L) {
