@@ -97,6 +97,66 @@ def cpu_baseline(w, band):
     }
 
 
+COPY_BYTES = 1 << 30  # calibration copy: 1 GiB read + 1 GiB written
+
+
+def copy_calibrate():
+    """A plain device-to-device copy of COPY_BYTES, three times, so that rocprofv3's
+    FETCH_SIZE / WRITE_SIZE counters can be scaled against a known byte count."""
+    import torch
+    src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log("copied %d bytes x3" % COPY_BYTES)
+
+
+def traffic_summary(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, workload, out_path=TRAFFIC_FILE):
+    """Fold four rocprofv3 --pmc runs (FETCH_SIZE and WRITE_SIZE for this benchmark
+    and for the calibration copy) into HBM bytes per launch per kernel."""
+    import csv
+    import glob
+
+    def per_kernel(d, counter):
+        vals = {}
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            for r in csv.DictReader(open(f)):
+                if r["Counter_Name"] != counter:
+                    continue
+                name = r["Kernel_Name"]
+                for key in ("row_lse_kernel", "future_mass_kernel", "copy", "elementwise"):
+                    if key in name:
+                        vals.setdefault(key, []).append(float(r["Counter_Value"]))
+        return vals
+
+    def copy_factor(d, counter):
+        v = per_kernel(d, counter)
+        cands = v.get("copy") or v.get("elementwise") or []
+        kib = max(cands)  # the 1 GiB copy dominates any other copy-like launch
+        return (COPY_BYTES / 1024.0) / kib, kib
+
+    ff, fk = copy_factor(copy_fetch_dir, "FETCH_SIZE")
+    wf, wk = copy_factor(copy_write_dir, "WRITE_SIZE")
+    fetch = per_kernel(fetch_dir, "FETCH_SIZE")
+    write = per_kernel(write_dir, "WRITE_SIZE")
+    kernels = {}
+    for k in ("row_lse_kernel", "future_mass_kernel"):
+        if k in fetch and k in write:
+            fb = sum(fetch[k]) / len(fetch[k]) * 1024.0 * ff
+            wb = sum(write[k]) / len(write[k]) * 1024.0 * wf
+            kernels[k] = {"fetch_bytes_per_launch": fb, "write_bytes_per_launch": wb,
+                          "hbm_bytes_per_launch": fb + wb, "launches": len(fetch[k])}
+    res = {"workload": workload, "kernel_source_sha256": kernel_source_hash(),
+           "copy_calibration": {"bytes": COPY_BYTES, "fetch_kib_read": fk, "write_kib_read": wk,
+                                "fetch_factor": ff, "write_factor": wf},
+           "kernels": kernels}
+    with open(out_path, "w") as f:
+        json.dump(res, f, indent=1)
+    print(json.dumps(res, indent=1))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -104,7 +164,17 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="qwen3_8b_t32k")
     ap.add_argument("--skip-cpu", action="store_true", help="omit the CPU oracle baseline")
+    ap.add_argument("--copy-calibrate", action="store_true",
+                    help="only run the 1 GiB calibration copy (for rocprofv3 FETCH_SIZE/WRITE_SIZE scaling)")
+    ap.add_argument("--traffic-summary", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
+                    help="fold rocprofv3 counter CSVs into profiles/hbm_traffic.json and exit")
     args = ap.parse_args()
+    if args.traffic_summary:
+        traffic_summary(*args.traffic_summary, workload=args.config)
+        return
+    if args.copy_calibrate:
+        copy_calibrate()
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU only: the future-attention target runs on a single MI355X "
               "(every (batch, KV head) group is independent; see the sharding design). Use --gpus 1.",

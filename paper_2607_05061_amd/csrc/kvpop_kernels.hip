@@ -264,13 +264,13 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
     }
   };
 
-  // Fast path: units v = (tile u, subtile n) as a software pipeline with a fixed
-  // issue order (scheduling barriers keep the compiler from regrouping it): k-step
-  // ks of unit v issues its MFMA, refills the A fragment register it consumed with
-  // the operand of unit v + 1 (used KS MFMAs later, hiding the LDS latency), and
-  // does the exp/accumulate work of 16 / KS elements of unit v - 1.
+  // Fast path: a software pipeline over the KT key tiles of the step with a fixed
+  // issue order (scheduling barriers keep the compiler from regrouping it). Tile
+  // u's unit runs the NQ MFMA chains of this wave's query subtiles interleaved
+  // k-step by k-step, so each A fragment read from LDS feeds NQ MFMAs; the fragment
+  // register is then refilled with tile u + 1's operand (used a whole unit later),
+  // and the exp/accumulate work of tile u - 1 fills the VALU slots in between.
   auto fast_step = [&](const uint16_t* sk, const float* sb) __attribute__((always_inline)) {
-    constexpr int U = KT * NQ;
     constexpr int EPK = 16 / KS;
     float nm[NQ];
 #pragma unroll
@@ -279,35 +279,47 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
     bf16x8 fr[KS];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) fr[ks] = TL::frag(sk, lane, ks);
-    f32x16 acc_prev;
+    f32x16 acc_prev[NQ];
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int v = 0; v <= U; ++v) {
-      const int u = v / NQ, n = v % NQ, un = (v + 1) / NQ, np = (v + NQ - 1) % NQ;
-      f32x16 acc = v < U ? acc_init(sb, u) : f32x16{};
-      float ts0 = 0.f, ts1 = 0.f;
+    for (int u = 0; u <= KT; ++u) {
+      f32x16 acc[NQ];
+      if (u < KT) {
+        const f32x16 a0 = acc_init(sb, u);
+#pragma unroll
+        for (int n = 0; n < NQ; ++n) acc[n] = a0;
+      }
+      float ts[NQ][2];
+#pragma unroll
+      for (int n = 0; n < NQ; ++n) ts[n][0] = ts[n][1] = 0.f;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        if (v < U) {
-          acc = mfma32(fr[ks], qf[n][ks], acc);
-          if (v + 1 < U) fr[ks] = TL::frag(sk + un * TL::ELEMS, lane, ks);
-        }
-        if (v > 0) {
+        if (u < KT) {
 #pragma unroll
-          for (int e = 0; e < EPK; ++e) {
-            const int r = ks * EPK + e;
-            const float x = exp2_fast(__builtin_fmaf(acc_prev[r], c, nm[np]));
-            if (e & 1) ts1 += x; else ts0 += x;
-          }
+          for (int n = 0; n < NQ; ++n) acc[n] = mfma32(fr[ks], qf[n][ks], acc[n]);
+          if (u + 1 < KT) fr[ks] = TL::frag(sk + (u + 1) * TL::ELEMS, lane, ks);
+        }
+        if (u > 0) {
+#pragma unroll
+          for (int n = 0; n < NQ; ++n)
+#pragma unroll
+            for (int e = 0; e < EPK; ++e) {
+              const int r = ks * EPK + e;
+              ts[n][e & 1] += exp2_fast(__builtin_fmaf(acc_prev[n][r], c, nm[n]));
+            }
         }
         __builtin_amdgcn_sched_barrier(0);
       }
-      if (v > 0) {
-        const float ts = ts0 + ts1;
-        sum[np] += ts;
-        ovf |= !(ts <= kOverflow);
+      if (u > 0) {
+#pragma unroll
+        for (int n = 0; n < NQ; ++n) {
+          const float t = ts[n][0] + ts[n][1];
+          sum[n] += t;
+          ovf |= !(t <= kOverflow);
+        }
       }
-      acc_prev = acc;
+#pragma unroll
+      for (int n = 0; n < NQ; ++n) acc_prev[n] = acc[n];
     }
     return ovf;
   };
@@ -482,48 +494,56 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
       cs += ts;
     };
 
-    // Fully admissible step: U = GC * NS units (head g, key subtile n) of KS MFMAs
-    // each, as a software pipeline whose issue order is fixed group by group (the
-    // scheduling barriers stop the compiler from regrouping it): k-step ks of unit
-    // u issues its MFMA, refills the A fragment register it just consumed with the
-    // operand of unit u + 1 (used KS MFMAs later, so the LDS latency is hidden),
-    // and does the exp/accumulate work of 16 / KS elements of unit u - 1, whose
-    // accumulators completed long before.
+    // Fully admissible step, as a software pipeline over the GC heads with a fixed
+    // issue order (the scheduling barriers stop the compiler from regrouping it).
+    // Head g's unit runs the NS MFMA chains of its key subtiles interleaved k-step
+    // by k-step, so each A fragment read from LDS feeds NS MFMAs; right after those
+    // MFMAs the fragment register is refilled with head g + 1's operand (used a
+    // whole unit later, hiding the LDS latency), and the exp/accumulate work of
+    // head g - 1, whose accumulators completed during the previous unit, fills the
+    // VALU slots in between.
     auto full_step = [&](const uint16_t* sq, const float* sl) __attribute__((always_inline)) {
-      constexpr int U = GC * NS;
-      constexpr int EPK = 16 / KS;  // elements of the previous unit per k-step
+      constexpr int EPK = 16 / KS;  // elements per subtile of the previous head per k-step
       bf16x8 fr[KS];
       float nl[2][16];
-      f32x16 acc_prev;
+      f32x16 acc_prev[NS];
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) fr[ks] = TL::frag(sq, lane, ks);
       read_nl(sl, 0, nl[0]);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int u = 0; u <= U; ++u) {
-        const int g = u / NS, n = u % NS, gn = (u + 1) / NS;
-        const int gp = (u - 1) / NS, np = (u - 1) % NS;
-        if (u > 0 && u < U && n == 0) read_nl(sl, g, nl[g & 1]);
-        f32x16 acc = f32x16{};
-        float ts0 = 0.f, ts1 = 0.f;
+      for (int g = 0; g <= GC; ++g) {
+        if (g > 0 && g < GC) read_nl(sl, g, nl[g & 1]);
+        f32x16 acc[NS];
+#pragma unroll
+        for (int n = 0; n < NS; ++n) acc[n] = f32x16{};
+        float ts[NS][2];
+#pragma unroll
+        for (int n = 0; n < NS; ++n) ts[n][0] = ts[n][1] = 0.f;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-          if (u < U) {
-            acc = mfma32(fr[ks], kf[n % NS][ks], acc);
-            if (u + 1 < U) fr[ks] = TL::frag(sq + gn * TL::ELEMS, lane, ks);
-          }
-          if (u > 0) {
+          if (g < GC) {
 #pragma unroll
-            for (int e = 0; e < EPK; ++e) {
-              const int r = ks * EPK + e;
-              const float x = exp2_fast(__builtin_fmaf(acc_prev[r], c, nl[gp & 1][r]));
-              if (e & 1) ts1 += x; else ts0 += x;
-            }
+            for (int n = 0; n < NS; ++n) acc[n] = mfma32(fr[ks], kf[n][ks], acc[n]);
+            if (g + 1 < GC) fr[ks] = TL::frag(sq + (g + 1) * TL::ELEMS, lane, ks);
+          }
+          if (g > 0) {
+#pragma unroll
+            for (int n = 0; n < NS; ++n)
+#pragma unroll
+              for (int e = 0; e < EPK; ++e) {
+                const int r = ks * EPK + e;
+                ts[n][e & 1] += exp2_fast(__builtin_fmaf(acc_prev[n][r], c, nl[(g - 1) & 1][r]));
+              }
           }
           __builtin_amdgcn_sched_barrier(0);
         }
-        if (u > 0) colsum[gp][np] += ts0 + ts1;
-        acc_prev = acc;
+        if (g > 0) {
+#pragma unroll
+          for (int n = 0; n < NS; ++n) colsum[g - 1][n] += ts[n][0] + ts[n][1];
+        }
+#pragma unroll
+        for (int n = 0; n < NS; ++n) acc_prev[n] = acc[n];
       }
     };
 
