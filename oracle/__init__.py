@@ -16,6 +16,9 @@ What it computes (paper, App. D.1, eqs. dense_logit_app .. future_mass_app):
 plus the transposed log-space form of App. D.2 (eq. future_mass_lse_app), used as an
 independent cross-check of the same quantity.
 
+The target epilogue of App. D.4 step 5 (aggregation over the G query heads and
+count normalisation, App. B.1-B.2) is in ``oracle.target``.
+
 Every function here is pinned by tests against closed forms, hand enumeration and
 brute force (tests/test_oracle_pins.py); no function is "parity unpinned".
 """
@@ -30,3 +33,4 @@ from .future_mass import (  # noqa: F401
     row_lse_blocked,
     row_lse_rows,
 )
+from .target import future_count, target_scores  # noqa: F401
