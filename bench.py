@@ -242,6 +242,28 @@ def main():
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic_for(name, w.name),
                 "kernel": name, "avg_launch_ms": round(dur, 4)}
 
+    # The same step with the target epilogue fused into pass 2 (App. D.4 step 5):
+    # per-KV-head scores log(max_g m_bar + eps) - log N_t instead of per-head masses.
+    scores = torch.empty((w.B, w.Hkv, w.T), dtype=torch.float32, device=dev)
+
+    def step_scores(evs):
+        evs[0].record()
+        kv.kvpop_row_lse(q, k, w.scale, key_bias=bias, lse=lse)
+        evs[1].record()
+        win, hor = w.bands[0]
+        kv.kvpop_future_attn_scores(q, k, lse, w.scale, win, hor, agg="max", eps=1e-8, normalize=True,
+                                    key_bias=bias, scores=scores)
+        evs[2].record()
+
+    n_epi = max(1, args.steps // 2)
+    evs2 = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n_epi)]
+    for s in range(n_epi):
+        step_scores(evs2[s])
+    torch.cuda.synchronize()
+    epi = {"band": list(w.bands[0]), "agg": "max", "steps": n_epi,
+           "ms_per_step": round(evs2[0][0].elapsed_time(evs2[-1][-1]) / n_epi, 4),
+           "pass2_with_epilogue_ms": round(float(np.mean([e[1].elapsed_time(e[2]) for e in evs2])), 4)}
+
     # Parity sanity on the live result: full-future masses of a head sum to T.
     for i, (a, b) in enumerate(w.bands):
         if a == 0 and b < 0:
@@ -274,6 +296,7 @@ def main():
         "pass_ms": {"row_lse": round(p1_ms, 4), "future_mass": [round(x, 4) for x in p2_ms]},
         "wall_s": round(wall, 3),
         "roofline": roofline,
+        "target_epilogue": epi,
         "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)

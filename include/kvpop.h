@@ -66,7 +66,8 @@ enum {
   KVPOP_OK = 0,
   KVPOP_EINVAL = 1,       /* NULL required pointer, non-positive dimension, Hq % Hkv != 0,
                              window < 0, 0 <= horizon < window, scale not finite and > 0,
-                             or a size whose element count overflows int64 */
+                             a bad epilogue option (agg, eps, normalize), overlapping
+                             buffers, or a size whose element count overflows int64 */
   KVPOP_EUNSUPPORTED = 2, /* head_dim not in {64, 128}, a base pointer not 16-byte
                              aligned, or T above KVPOP_MAX_SEQ_LEN */
   KVPOP_EHIP = 3          /* the HIP runtime reported an error while launching;
@@ -110,6 +111,27 @@ int kvpop_future_attn_from_lse(const kvpop_dims* dims, const void* q, const void
 int kvpop_future_attn_target(const kvpop_dims* dims, const void* q, const void* k,
                              const float* key_bias, int32_t window, int32_t horizon,
                              float* lse_ws, float* out, void* stream);
+
+/* Aggregation over the G query heads of a KV head (App. B.1). */
+enum {
+  KVPOP_AGG_MAX = 0,  /* eq. max_group_aggregation_app: the paper's default */
+  KVPOP_AGG_MEAN = 1  /* eq. mean_group_aggregation_app: probability-space mean */
+};
+
+/* Pass 2 plus the target epilogue (App. D.4 step 5; App. B.1-B.2): the per-KV-head
+ * target score
+ *   scores[b, h, t] = log(A_t + eps) - (normalize ? log N_t : 0),
+ *   A_t = max_g out[b, h*G + g, t]  (agg = KVPOP_AGG_MAX)  or  mean_g (KVPOP_AGG_MEAN),
+ *   N_t = max(1, |band(t)|)  (eq. future_count_app, clipped by the lookahead),
+ * where out is the future mass of kvpop_future_attn_from_lse on the same
+ * arguments. eps is added to the aggregated, unnormalised mass before the
+ * logarithm, in the order of App. B (the paper leaves eps's value open; it must be
+ * finite and >= 0). lse: fp32 [B,Hq,T] (as for kvpop_future_attn_from_lse).
+ * out: fp32 [B,Hq,T] per-head masses, or NULL to skip writing them.
+ * scores: fp32 [B,Hkv,T] output. normalize: 0 or 1. */
+int kvpop_future_attn_scores(const kvpop_dims* dims, const void* q, const void* k, const float* key_bias,
+                             const float* lse, int32_t window, int32_t horizon, int32_t agg, float eps,
+                             int32_t normalize, float* out, float* scores, void* stream);
 
 /* Human-readable text for a status code. For KVPOP_EHIP it is the HIP runtime's
  * message for the last failure on the calling thread. Never returns NULL; the

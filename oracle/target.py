@@ -46,7 +46,8 @@ def target_scores(m_bar, n_kv_heads: int, window: int, horizon: int, agg: str = 
         m_agg = grouped.mean(axis=2)
     else:
         raise ValueError("agg must be 'max' or 'mean'")
-    r = np.log(m_agg + eps)
+    with np.errstate(divide="ignore"):  # eps = 0 and an empty band give log(0) = -inf
+        r = np.log(m_agg + eps)
     if normalize:
         r = r - np.log(future_count(T, window, horizon))[None, None, :]
     return r

@@ -23,13 +23,15 @@ from typing import Optional, Tuple
 __all__ = [
     "KVPOP_OK", "KVPOP_EINVAL", "KVPOP_EUNSUPPORTED", "KVPOP_EHIP", "KvpopDims", "KvpopError",
     "lib", "lib_path", "kvpop_row_lse", "kvpop_future_attn_from_lse", "kvpop_future_attn_target",
-    "kvpop_strerror", "kvpop_abi_version",
+    "kvpop_future_attn_scores", "kvpop_strerror", "kvpop_abi_version", "KVPOP_AGG_MAX", "KVPOP_AGG_MEAN",
 ]
 
 KVPOP_OK = 0
 KVPOP_EINVAL = 1
 KVPOP_EUNSUPPORTED = 2
 KVPOP_EHIP = 3
+KVPOP_AGG_MAX = 0
+KVPOP_AGG_MEAN = 1
 ABI_VERSION = 1
 
 _PKG_DIR = os.path.dirname(os.path.abspath(__file__))
@@ -75,6 +77,8 @@ def lib() -> ctypes.CDLL:
         L.kvpop_future_attn_from_lse.restype = ctypes.c_int
         L.kvpop_future_attn_target.argtypes = [D, P, P, P, I32, I32, P, P, P]
         L.kvpop_future_attn_target.restype = ctypes.c_int
+        L.kvpop_future_attn_scores.argtypes = [D, P, P, P, P, I32, I32, I32, F, I32, P, P, P]
+        L.kvpop_future_attn_scores.restype = ctypes.c_int
         L.kvpop_strerror.argtypes = [ctypes.c_int]
         L.kvpop_strerror.restype = ctypes.c_char_p
         L.kvpop_abi_version.argtypes = []
@@ -191,3 +195,29 @@ def kvpop_future_attn_target(q, k, scale: float, window: int = 0, horizon: int =
     if st != KVPOP_OK:
         raise KvpopError(st, "kvpop_future_attn_target")
     return out, lse_ws
+
+
+def kvpop_future_attn_scores(q, k, lse, scale: float, window: int = 0, horizon: int = -1, agg: str = "max",
+                             eps: float = 1e-8, normalize: bool = True, key_bias=None, scores=None, out=None,
+                             write_mass: bool = False, stream=None):
+    """Pass 2 plus the target epilogue (App. D.4 step 5): per-KV-head scores
+    log(agg_g m_bar + eps) - log N_t, fp32 [B, Hkv, T]. Returns (scores, out), where
+    out holds the per-head masses if ``write_mass`` (or ``out``) is given, else None."""
+    torch = _torch()
+    d = _dims(q, k, scale)
+    qp, kp, bp = _prep_inputs(q, k, key_bias)
+    _check_tensor(lse, "lse", torch.float32, q.device)
+    if tuple(lse.shape) != (d.batch, d.n_q_heads, d.seq_len):
+        raise ValueError("lse must be [B, Hq, T]")
+    if agg not in ("max", "mean"):
+        raise ValueError("agg must be 'max' or 'mean'")
+    scores = _prep_out(scores, "scores", (d.batch, d.n_kv_heads, d.seq_len), q.device)
+    if out is not None or write_mass:
+        out = _prep_out(out, "out", (d.batch, d.n_q_heads, d.seq_len), q.device)
+    st = lib().kvpop_future_attn_scores(ctypes.byref(d), qp, kp, bp, lse.data_ptr(), int(window), int(horizon),
+                                        KVPOP_AGG_MAX if agg == "max" else KVPOP_AGG_MEAN, float(eps),
+                                        int(bool(normalize)), out.data_ptr() if out is not None else None,
+                                        scores.data_ptr(), _stream_ptr(stream, q.device))
+    if st != KVPOP_OK:
+        raise KvpopError(st, "kvpop_future_attn_scores")
+    return scores, out

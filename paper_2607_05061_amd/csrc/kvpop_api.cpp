@@ -152,6 +152,39 @@ int kvpop_future_attn_from_lse(const kvpop_dims* dims, const void* q, const void
   return hip_status(kvpop::launch_future_mass(L));
 }
 
+int kvpop_future_attn_scores(const kvpop_dims* dims, const void* q, const void* k, const float* key_bias,
+                             const float* lse, int32_t window, int32_t horizon, int32_t agg, float eps,
+                             int32_t normalize, float* out, float* scores, void* stream) {
+  Sizes sz;
+  int st = check_inputs(dims, q, k, key_bias, &sz);
+  if (st != KVPOP_OK) return st;
+  if (!lse) return KVPOP_EINVAL;
+  if (!aligned16(lse)) return KVPOP_EUNSUPPORTED;
+  st = check_band(window, horizon);
+  if (st != KVPOP_OK) return st;
+  if ((agg != KVPOP_AGG_MAX && agg != KVPOP_AGG_MEAN) || (normalize != 0 && normalize != 1) || !std::isfinite(eps) ||
+      eps < 0.f)
+    return KVPOP_EINVAL;
+  const int64_t score_bytes = (int64_t)dims->batch * dims->n_kv_heads * dims->seq_len * 4;
+  st = check_output(scores, score_bytes, sz, dims, q, k, key_bias, lse, sz.row_elems * 4);
+  if (st != KVPOP_OK) return st;
+  if (out) {
+    st = check_output(out, sz.row_elems * 4, sz, dims, q, k, key_bias, lse, sz.row_elems * 4);
+    if (st != KVPOP_OK) return st;
+    if (overlap(out, sz.row_elems * 4, scores, score_bytes)) return KVPOP_EINVAL;
+  }
+  kvpop::Launch L = make_launch(dims, q, k, key_bias, stream);
+  L.lse = lse;
+  L.out = out;
+  L.window = window;
+  L.horizon = horizon;
+  L.scores = scores;
+  L.agg = agg;
+  L.eps = eps;
+  L.normalize = normalize;
+  return hip_status(kvpop::launch_future_mass(L));
+}
+
 int kvpop_future_attn_target(const kvpop_dims* dims, const void* q, const void* k, const float* key_bias,
                              int32_t window, int32_t horizon, float* lse_ws, float* out, void* stream) {
   Sizes sz;

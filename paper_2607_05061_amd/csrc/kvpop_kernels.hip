@@ -385,12 +385,18 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
 // Query rows beyond T get LSE = +inf in LDS, which zeroes their terms. A per-key
 // bias is factored out of the sum, out_t = exp(bias_t) * sum_d exp(...). Query
 // heads are processed GC at a time; G / GC chunks each repeat the sweep.
+//
+// With EPI the kernel also finishes the target (App. D.4 step 5, App. B.1-B.2):
+// it folds the G per-head masses of each key into their max or sum as the chunks
+// complete, and writes log(agg + eps) - log N_t per KV head, where N_t = max(1,
+// number of admissible queries). The per-head masses are then written only when
+// `out` is given.
 // ---------------------------------------------------------------------------
-template <int D, int NS, int GC, bool HAS_BIAS>
+template <int D, int NS, int GC, bool HAS_BIAS, bool EPI>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2))) void
 future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const float* __restrict__ bias,
                    const float* __restrict__ lse, float* __restrict__ out, int B, int Hq, int Hkv, int T, float c,
-                   int window, int hz) {
+                   int window, int hz, float* __restrict__ scores, int agg_mean, float eps, int normalize) {
   using TL = Tile<D>;
   constexpr int KS = TL::KS;
   constexpr int WK = NS * 32;  // keys per wave
@@ -433,15 +439,36 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     }
   }
 
-  if (nqt == 0) {
-    // Every key of the block has an empty query range.
-    for (int g = 0; g < G; ++g) {
+  float aggv[NS];  // running max or sum over query heads (EPI)
 #pragma unroll
-      for (int n = 0; n < NS; ++n) {
-        const int j = jw + 32 * n + l32;
-        if (hi == 0 && j < T) out[(size_t)(b * Hq + h * G + g) * T + j] = 0.f;
+  for (int n = 0; n < NS; ++n) aggv[n] = 0.f;
+  auto write_scores = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int n = 0; n < NS; ++n) {
+      const int j = jw + 32 * n + l32;
+      if (hi == 0 && j < T) {
+        float r = __logf((agg_mean ? aggv[n] / (float)G : aggv[n]) + eps);
+        if (normalize) {
+          const long long cnt = min((long long)T - 1, (long long)j + hz) - ((long long)j + window) + 1;
+          r -= __logf((float)max(1LL, cnt));
+        }
+        scores[(size_t)bh * T + j] = r;
       }
     }
+  };
+
+  if (nqt == 0) {
+    // Every key of the block has an empty query range.
+    if (!EPI || out) {
+      for (int g = 0; g < G; ++g) {
+#pragma unroll
+        for (int n = 0; n < NS; ++n) {
+          const int j = jw + 32 * n + l32;
+          if (hi == 0 && j < T) out[(size_t)(b * Hq + h * G + g) * T + j] = 0.f;
+        }
+      }
+    }
+    if (EPI) write_scores();
     return;
   }
 
@@ -600,12 +627,15 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     for (int g = 0; g < GC; ++g) {
 #pragma unroll
       for (int n = 0; n < NS; ++n) {
-        const float v = colsum[g][n] + __shfl_xor(colsum[g][n], 32);
+        float v = colsum[g][n] + __shfl_xor(colsum[g][n], 32);
+        if (HAS_BIAS) v *= fac[n];
         const int j = jw + 32 * n + l32;
-        if (hi == 0 && j < T) out[(head0 + g) * T + j] = HAS_BIAS ? v * fac[n] : v;
+        if (hi == 0 && j < T && (!EPI || out)) out[(head0 + g) * T + j] = v;
+        if (EPI) aggv[n] = agg_mean ? aggv[n] + v : fmaxf(aggv[n], v);
       }
     }
   }
+  if (EPI) write_scores();
 }
 
 template <int D, int P, bool HB>
@@ -636,22 +666,24 @@ int launch_p1_d(const Launch& L) {
   return launch_p1_b<D, 1>(L);
 }
 
-template <int D, int NS, int GC, bool HB>
+template <int D, int NS, int GC, bool HB, bool EPI>
 int launch_p2(const Launch& L) {
   constexpr int BK = 4 * NS * 32;
   const int nkb = (L.T + BK - 1) / BK;
   const long long grid = (long long)nkb * L.B * L.Hkv;
   const float c = L.scale * kLog2e;
   const int hz = L.horizon < 0 ? L.T : L.horizon;
-  hipLaunchKernelGGL((future_mass_kernel<D, NS, GC, HB>), dim3((unsigned)grid), dim3(256), 0, (hipStream_t)L.stream,
-                     reinterpret_cast<const uint16_t*>(L.q), reinterpret_cast<const uint16_t*>(L.k), L.bias, L.lse,
-                     L.out, L.B, L.Hq, L.Hkv, L.T, c, L.window, hz);
+  hipLaunchKernelGGL((future_mass_kernel<D, NS, GC, HB, EPI>), dim3((unsigned)grid), dim3(256), 0,
+                     (hipStream_t)L.stream, reinterpret_cast<const uint16_t*>(L.q),
+                     reinterpret_cast<const uint16_t*>(L.k), L.bias, L.lse, L.out, L.B, L.Hq, L.Hkv, L.T, c, L.window,
+                     hz, L.scores, L.agg, L.eps, L.normalize);
   return (int)hipGetLastError();
 }
 
 template <int D, int NS, int GC>
 int launch_p2_b(const Launch& L) {
-  return L.bias ? launch_p2<D, NS, GC, true>(L) : launch_p2<D, NS, GC, false>(L);
+  if (L.scores) return L.bias ? launch_p2<D, NS, GC, true, true>(L) : launch_p2<D, NS, GC, false, true>(L);
+  return L.bias ? launch_p2<D, NS, GC, true, false>(L) : launch_p2<D, NS, GC, false, false>(L);
 }
 
 template <int D, int NS>

@@ -25,7 +25,7 @@ def _declared_functions():
 def test_header_declares_the_entry_points():
     names = set(_declared_functions())
     assert names == {"kvpop_row_lse", "kvpop_future_attn_from_lse", "kvpop_future_attn_target",
-                     "kvpop_strerror", "kvpop_abi_version"}
+                     "kvpop_future_attn_scores", "kvpop_strerror", "kvpop_abi_version"}
 
 
 def test_library_exports_every_declared_symbol():
@@ -69,10 +69,15 @@ def _tgt(d, q=A, k=B_, bias=None, w=0, h=-1, ws=C_, out=D_):
                                              None)
 
 
+def _sc(d, q=A, k=B_, bias=None, lse=C_, w=0, h=-1, agg=0, eps=1e-8, norm=1, out=None, scores=D_):
+    return kv.lib().kvpop_future_attn_scores(ctypes.byref(d) if d is not None else None, q, k, bias, lse, w, h, agg,
+                                             eps, norm, out, scores, None)
+
+
 EINVAL, EUNS = kv.KVPOP_EINVAL, kv.KVPOP_EUNSUPPORTED
 
 
-@pytest.mark.parametrize("call", [_lse, _p2, _tgt])
+@pytest.mark.parametrize("call", [_lse, _p2, _tgt, _sc])
 def test_bad_dims(call):
     assert call(None) == EINVAL
     for kw in (dict(B=0), dict(Hq=0), dict(Hkv=0), dict(T=0), dict(D=0), dict(B=-1), dict(T=-5)):
@@ -85,7 +90,7 @@ def test_bad_dims(call):
     assert call(_dims(T=(1 << 24) + 1)) == EUNS
 
 
-@pytest.mark.parametrize("call", [_lse, _p2, _tgt])
+@pytest.mark.parametrize("call", [_lse, _p2, _tgt, _sc])
 def test_null_and_misaligned_pointers(call):
     d = _dims()
     assert call(d, q=None) == EINVAL
@@ -114,7 +119,23 @@ def test_overlapping_buffers_rejected():
     assert _p2(d, bias=E_, out=E_) == EINVAL        # out over the bias
 
 
-@pytest.mark.parametrize("call", [_p2, _tgt])
+def test_epilogue_option_checks():
+    d = _dims()
+    assert _sc(d, agg=2) == EINVAL
+    assert _sc(d, agg=-1) == EINVAL
+    assert _sc(d, norm=2) == EINVAL
+    assert _sc(d, eps=-1e-3) == EINVAL
+    assert _sc(d, eps=math.inf) == EINVAL
+    assert _sc(d, eps=math.nan) == EINVAL
+    assert _sc(d, scores=None) == EINVAL
+    assert _sc(d, scores=D_ + 4) == EUNS
+    assert _sc(d, lse=None) == EINVAL
+    assert _sc(d, out=D_ + 64) == EINVAL          # out overlaps scores
+    assert _sc(d, scores=C_ + 16) == EINVAL       # scores inside lse
+    assert _sc(d, out=E_ + 8) == EUNS             # misaligned optional out
+
+
+@pytest.mark.parametrize("call", [_p2, _tgt, _sc])
 def test_bad_bands(call):
     d = _dims()
     assert call(d, w=-1) == EINVAL
