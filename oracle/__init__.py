@@ -16,6 +16,10 @@ What it computes (paper, App. D.1, eqs. dense_logit_app .. future_mass_app):
 plus the transposed log-space form of App. D.2 (eq. future_mass_lse_app), used as an
 independent cross-check of the same quantity.
 
+The running top-k policy pieces (static priorities, ranks, cutoffs, the sparse
+mask and the sparse log-normaliser of App. C and App. D.3) are in
+``oracle.running_topk``.
+
 The target epilogue of App. D.4 step 5 (aggregation over the G query heads and
 count normalisation, App. B.1-B.2) is in ``oracle.target``.
 
@@ -34,3 +38,11 @@ from .future_mass import (  # noqa: F401
     row_lse_rows,
 )
 from .target import future_count, target_scores  # noqa: F401
+from .running_topk import (  # noqa: F401
+    ranks_from_priority,
+    running_cutoff_bruteforce,
+    running_cutoff_fenwick,
+    running_topk_mask,
+    sparse_row_lse,
+    static_priority,
+)
