@@ -45,4 +45,6 @@ from .running_topk import (  # noqa: F401
     running_topk_mask,
     sparse_row_lse,
     static_priority,
+    static_priority_f32,
+    teacher_labels,
 )

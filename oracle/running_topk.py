@@ -26,14 +26,24 @@ import numpy as np
 
 from .future_mass import _as_f64
 
-__all__ = ["static_priority", "ranks_from_priority", "running_cutoff_bruteforce", "running_cutoff_fenwick",
-           "running_topk_mask", "sparse_row_lse"]
+__all__ = ["static_priority", "static_priority_f32", "ranks_from_priority", "running_cutoff_bruteforce",
+           "running_cutoff_fenwick", "running_topk_mask", "sparse_row_lse", "teacher_labels"]
 
 
 def static_priority(r, log_gamma: float) -> np.ndarray:
     """r_bar_t = r_t - t * log(gamma) for decay step 1 (eq. static_priority_app)."""
     r = np.asarray(r, dtype=np.float64)
     return r - np.arange(r.shape[-1], dtype=np.float64) * float(log_gamma)
+
+
+def static_priority_f32(r, log_gamma: float) -> np.ndarray:
+    """The same static priority evaluated in float32, one rounding per operation:
+    fl(r_t - fl(t * log_gamma)). The paper computes decay and top-k ranking in
+    float32 (App. F), and the ranking is an integer decided by these values, so the
+    oracle takes that decision in the same precision as the GPU."""
+    r32 = np.asarray(r, dtype=np.float32)
+    t32 = np.arange(r32.shape[-1], dtype=np.float32)
+    return r32 - t32 * np.float32(log_gamma)
 
 
 def ranks_from_priority(prio) -> np.ndarray:
@@ -132,3 +142,27 @@ def sparse_row_lse(q, k, scale: float, mask, bias=None) -> np.ndarray:
     L = np.where(np.asarray(mask, dtype=bool), L, -np.inf)
     mx = L.max(axis=1)
     return mx + np.log(np.sum(np.exp(L - mx[:, None]), axis=1))
+
+
+def teacher_labels(rank, tau, s: int, w: int):
+    """Teacher label and boundary token per query (Sec. 3.1 eq. teacher_label).
+
+    t_new = q - w is the newly eligible token; the teacher keeps the eligible tokens
+    with rank <= tau_q (all of them while |E(q)| < k). y_q = +1 if t_new is kept,
+    -1 otherwise; t_bnd is the kept eligible token with the largest rank (the
+    boundary of the kept set). Queries with an empty eligible set get y = 0 and
+    t_bnd = -1."""
+    rank = np.asarray(rank)
+    tau = np.asarray(tau)
+    T = rank.shape[0]
+    y = np.zeros(T, dtype=np.int64)
+    t_bnd = np.full(T, -1, dtype=np.int64)
+    for q in range(T):
+        hi = q - w
+        if hi < s:
+            continue
+        elig = np.arange(s, hi + 1)
+        kept = elig[rank[elig] <= tau[q]]
+        t_bnd[q] = kept[np.argmax(rank[kept])]
+        y[q] = 1 if rank[hi] <= tau[q] else -1
+    return y, t_bnd

@@ -104,3 +104,36 @@ def test_sparse_lse_brute_force():
     for d in range(T):
         want = math.log(sum(math.exp(0.7 * float(q[d] @ k[t])) for t in range(T) if M[d, t]))
         assert got[d] == pytest.approx(want, rel=1e-13)
+
+
+def test_teacher_labels_hand_case():
+    """ranks (0, 3, 1, 4, 2), s=1, w=1, k=2: cutoffs (T, T, T, 3, 3).
+    q=2: E={1}, kept all, t_new=1 kept (+1), boundary 1.
+    q=3: E={1,2} ranks {3,1}, tau=3: both kept; t_new=2 (+1); boundary = rank 3 -> t=1.
+    q=4: E={1,2,3} ranks {3,1,4}, tau=3: t_new=3 has rank 4 > 3 (-1); boundary t=1."""
+    rank = np.array([0, 3, 1, 4, 2])
+    tau = oracle.running_cutoff_bruteforce(rank, 1, 1, 2)
+    y, tb = oracle.teacher_labels(rank, tau, 1, 1)
+    np.testing.assert_array_equal(y, [0, 0, 1, 1, -1])
+    np.testing.assert_array_equal(tb, [-1, -1, 1, 1, 1])
+
+
+def test_teacher_labels_properties():
+    T, s, w, k = 400, 4, 20, 30
+    rank = np.random.default_rng(11).permutation(T)
+    tau = oracle.running_cutoff_fenwick(rank, s, w, k)
+    y, tb = oracle.teacher_labels(rank, tau, s, w)
+    q = np.arange(T)
+    assert np.all(y[q - w < s] == 0) and np.all(tb[q - w < s] == -1)
+    sat = tau < T
+    np.testing.assert_array_equal(rank[tb[sat]], tau[sat])          # boundary has the cutoff rank
+    assert np.all(y[(q - w >= s) & ~sat] == 1)                       # budget not yet saturated
+    m = (q - w >= s) & sat
+    np.testing.assert_array_equal(y[m] == 1, rank[q[m] - w] <= tau[m])
+
+
+def test_f32_priority_rounding_is_per_operation():
+    r = np.array([1.0, 1.0, 1.0], dtype=np.float32)
+    p = oracle.static_priority_f32(r, -1e-3)
+    want = [np.float32(1.0) - np.float32(np.float32(t) * np.float32(-1e-3)) for t in range(3)]
+    np.testing.assert_array_equal(p, np.array(want, dtype=np.float32))
