@@ -53,6 +53,7 @@
 #ifndef KVPOP_H
 #define KVPOP_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -132,6 +133,46 @@ enum {
 int kvpop_future_attn_scores(const kvpop_dims* dims, const void* q, const void* k, const float* key_bias,
                              const float* lse, int32_t window, int32_t horizon, int32_t agg, float eps,
                              int32_t normalize, float* out, float* scores, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Running top-k ranking (App. B.3, App. C; Sec. 3.1 eqs. eligible_set and
+ * teacher_label). Independent of the attention passes: it works on one score per
+ * (batch row, KV head, position), either the target of kvpop_future_attn_scores
+ * (the teacher) or a scorer's prediction (the student's sparse mask).
+ *
+ * For each (b, h) sequence r[b, h, 0..T-1]:
+ *   prio_t   = fl(r_t - fl(t * log_gamma[h]))      float32, decay step 1
+ *              (eq. static_priority_app; log_gamma NULL means no decay)
+ *   rank_t   = position of t in descending prio order, ties to the smaller t
+ *              (rank 0 = highest priority)
+ *   E(q)     = {t : sinks <= t <= q - window}       (eq. eligible_set)
+ *   cutoff_q = the k-th smallest rank in E(q) if |E(q)| >= k, else T (every
+ *              eligible token kept); the retained long-range keys of query q are
+ *              the t in E(q) with rank_t <= cutoff_q (App. C.1 eq.
+ *              running_topk_mask_app, App. C.2)
+ *   label_q  = +1 if t_new = q - window is retained, -1 if not, 0 if E(q) is
+ *              empty (eq. teacher_label)
+ *   boundary_q = the retained token of E(q) with the largest rank (the teacher's
+ *              cutoff token t_bnd), -1 if E(q) is empty
+ * --------------------------------------------------------------------------- */
+typedef struct kvpop_topk_dims {
+  int32_t batch;    /* B >= 1 */
+  int32_t n_heads;  /* H >= 1 (KV heads) */
+  int32_t seq_len;  /* T >= 1, T <= KVPOP_MAX_SEQ_LEN */
+} kvpop_topk_dims;
+
+/* Bytes of device workspace kvpop_running_topk needs for these dimensions
+ * (0 if they are invalid). */
+size_t kvpop_running_topk_workspace_size(const kvpop_topk_dims* dims);
+
+/* scores: fp32 [B,H,T]; log_gamma: fp32 [H] or NULL; sinks >= 0, window >= 0,
+ * topk >= 1. Outputs int32 [B,H,T]: rank and cutoff (required), label and boundary
+ * (optional, NULL to skip). workspace: caller-allocated device memory of at least
+ * kvpop_running_topk_workspace_size bytes, 16-byte aligned; its contents on entry
+ * do not matter. All outputs are fully overwritten. */
+int kvpop_running_topk(const kvpop_topk_dims* dims, const float* scores, const float* log_gamma, int32_t sinks,
+                       int32_t window, int32_t topk, int32_t* rank, int32_t* cutoff, int32_t* label,
+                       int32_t* boundary, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Human-readable text for a status code. For KVPOP_EHIP it is the HIP runtime's
  * message for the last failure on the calling thread. Never returns NULL; the

@@ -144,20 +144,21 @@ def sparse_row_lse(q, k, scale: float, mask, bias=None) -> np.ndarray:
     return mx + np.log(np.sum(np.exp(L - mx[:, None]), axis=1))
 
 
-def teacher_labels(rank, tau, s: int, w: int):
+def teacher_labels(rank, tau, s: int, w: int, queries=None):
     """Teacher label and boundary token per query (Sec. 3.1 eq. teacher_label).
 
     t_new = q - w is the newly eligible token; the teacher keeps the eligible tokens
     with rank <= tau_q (all of them while |E(q)| < k). y_q = +1 if t_new is kept,
     -1 otherwise; t_bnd is the kept eligible token with the largest rank (the
     boundary of the kept set). Queries with an empty eligible set get y = 0 and
-    t_bnd = -1."""
+    t_bnd = -1. `queries` (optional) restricts the work to those query positions;
+    the others are left at y = 0, t_bnd = -1."""
     rank = np.asarray(rank)
     tau = np.asarray(tau)
     T = rank.shape[0]
     y = np.zeros(T, dtype=np.int64)
     t_bnd = np.full(T, -1, dtype=np.int64)
-    for q in range(T):
+    for q in (range(T) if queries is None else queries):
         hi = q - w
         if hi < s:
             continue

@@ -24,6 +24,7 @@ __all__ = [
     "KVPOP_OK", "KVPOP_EINVAL", "KVPOP_EUNSUPPORTED", "KVPOP_EHIP", "KvpopDims", "KvpopError",
     "lib", "lib_path", "kvpop_row_lse", "kvpop_future_attn_from_lse", "kvpop_future_attn_target",
     "kvpop_future_attn_scores", "kvpop_strerror", "kvpop_abi_version", "KVPOP_AGG_MAX", "KVPOP_AGG_MEAN",
+    "KvpopTopkDims", "kvpop_running_topk", "kvpop_running_topk_workspace_size",
 ]
 
 KVPOP_OK = 0
@@ -48,6 +49,11 @@ class KvpopDims(ctypes.Structure):
         ("head_dim", ctypes.c_int32),
         ("scale", ctypes.c_float),
     ]
+
+
+class KvpopTopkDims(ctypes.Structure):
+    """Mirror of ``kvpop_topk_dims`` in include/kvpop.h."""
+    _fields_ = [("batch", ctypes.c_int32), ("n_heads", ctypes.c_int32), ("seq_len", ctypes.c_int32)]
 
 
 class KvpopError(RuntimeError):
@@ -79,6 +85,11 @@ def lib() -> ctypes.CDLL:
         L.kvpop_future_attn_target.restype = ctypes.c_int
         L.kvpop_future_attn_scores.argtypes = [D, P, P, P, P, I32, I32, I32, F, I32, P, P, P]
         L.kvpop_future_attn_scores.restype = ctypes.c_int
+        L.kvpop_running_topk_workspace_size.argtypes = [ctypes.POINTER(KvpopTopkDims)]
+        L.kvpop_running_topk_workspace_size.restype = ctypes.c_size_t
+        L.kvpop_running_topk.argtypes = [ctypes.POINTER(KvpopTopkDims), P, P, I32, I32, I32, P, P, P, P, P,
+                                         ctypes.c_size_t, P]
+        L.kvpop_running_topk.restype = ctypes.c_int
         L.kvpop_strerror.argtypes = [ctypes.c_int]
         L.kvpop_strerror.restype = ctypes.c_char_p
         L.kvpop_abi_version.argtypes = []
@@ -221,3 +232,44 @@ def kvpop_future_attn_scores(q, k, lse, scale: float, window: int = 0, horizon: 
     if st != KVPOP_OK:
         raise KvpopError(st, "kvpop_future_attn_scores")
     return scores, out
+
+
+def kvpop_running_topk_workspace_size(batch: int, n_heads: int, seq_len: int) -> int:
+    d = KvpopTopkDims(batch, n_heads, seq_len)
+    return int(lib().kvpop_running_topk_workspace_size(ctypes.byref(d)))
+
+
+def kvpop_running_topk(scores, sinks: int, window: int, topk: int, log_gamma=None, labels: bool = True,
+                       workspace=None, stream=None):
+    """Ranks, running cutoffs and (optionally) teacher labels and boundary tokens for
+    scores [B, H, T] (App. B.3, App. C). Returns a dict of int32 tensors."""
+    torch = _torch()
+    _check_tensor(scores, "scores", torch.float32, None)
+    if scores.dim() != 3:
+        raise ValueError("scores must be [B, H, T]")
+    B, H, T = scores.shape
+    if log_gamma is not None:
+        _check_tensor(log_gamma, "log_gamma", torch.float32, scores.device)
+        if tuple(log_gamma.shape) != (H,):
+            raise ValueError("log_gamma must be [H]")
+    need = kvpop_running_topk_workspace_size(B, H, T)
+    if need == 0:
+        raise ValueError("invalid dimensions")
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=scores.device)
+    elif workspace.numel() * workspace.element_size() < need or workspace.device != scores.device:
+        raise ValueError("workspace must hold %d bytes on the device of scores" % need)
+    out = {n: torch.empty((B, H, T), dtype=torch.int32, device=scores.device) for n in ("rank", "cutoff")}
+    if labels:
+        out["label"] = torch.empty((B, H, T), dtype=torch.int32, device=scores.device)
+        out["boundary"] = torch.empty((B, H, T), dtype=torch.int32, device=scores.device)
+    d = KvpopTopkDims(B, H, T)
+    st = lib().kvpop_running_topk(ctypes.byref(d), scores.data_ptr(),
+                                  log_gamma.data_ptr() if log_gamma is not None else None, int(sinks), int(window),
+                                  int(topk), out["rank"].data_ptr(), out["cutoff"].data_ptr(),
+                                  out["label"].data_ptr() if labels else None,
+                                  out["boundary"].data_ptr() if labels else None, workspace.data_ptr(),
+                                  workspace.numel() * workspace.element_size(), _stream_ptr(stream, scores.device))
+    if st != KVPOP_OK:
+        raise KvpopError(st, "kvpop_running_topk")
+    return out

@@ -185,6 +185,59 @@ int kvpop_future_attn_scores(const kvpop_dims* dims, const void* q, const void* 
   return hip_status(kvpop::launch_future_mass(L));
 }
 
+size_t kvpop_running_topk_workspace_size(const kvpop_topk_dims* d) {
+  if (!d || d->batch < 1 || d->n_heads < 1 || d->seq_len < 1 || d->seq_len > KVPOP_MAX_SEQ_LEN) return 0;
+  const size_t seqs = (size_t)d->batch * (size_t)d->n_heads;
+  const size_t words = kvpop::topk_workspace_words_per_seq(d->seq_len);
+  if (seqs > SIZE_MAX / 4 / words) return 0;
+  return seqs * words * 4;
+}
+
+int kvpop_running_topk(const kvpop_topk_dims* d, const float* scores, const float* log_gamma, int32_t sinks,
+                       int32_t window, int32_t topk, int32_t* rank, int32_t* cutoff, int32_t* label,
+                       int32_t* boundary, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!d || d->batch < 1 || d->n_heads < 1 || d->seq_len < 1) return KVPOP_EINVAL;
+  if (d->seq_len > KVPOP_MAX_SEQ_LEN) return KVPOP_EUNSUPPORTED;
+  if (sinks < 0 || window < 0 || topk < 1) return KVPOP_EINVAL;
+  if (!scores || !rank || !cutoff || !workspace) return KVPOP_EINVAL;
+  const size_t need = kvpop_running_topk_workspace_size(d);
+  if (need == 0 || workspace_bytes < need) return KVPOP_EINVAL;
+  const void* ptrs[] = {scores, log_gamma, rank, cutoff, label, boundary, workspace};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return KVPOP_EUNSUPPORTED;
+  const int64_t n = (int64_t)d->batch * d->n_heads * d->seq_len;
+  if (n / d->seq_len / d->n_heads != d->batch || n * 4 > INT64_MAX / 2) return KVPOP_EINVAL;
+  const int64_t b = n * 4;
+  // Outputs must not overlap each other, the inputs or the workspace.
+  const void* outs[] = {rank, cutoff, label, boundary};
+  for (int i = 0; i < 4; ++i) {
+    if (!outs[i]) continue;
+    if (overlap(outs[i], b, scores, b) || overlap(outs[i], b, log_gamma, (int64_t)d->n_heads * 4) ||
+        overlap(outs[i], b, workspace, (int64_t)need))
+      return KVPOP_EINVAL;
+    for (int j = i + 1; j < 4; ++j)
+      if (overlap(outs[i], b, outs[j], b)) return KVPOP_EINVAL;
+  }
+  if (overlap(workspace, (int64_t)need, scores, b) || overlap(workspace, (int64_t)need, log_gamma, (int64_t)d->n_heads * 4))
+    return KVPOP_EINVAL;
+  kvpop::TopkLaunch L{};
+  L.scores = scores;
+  L.log_gamma = log_gamma;
+  L.B = d->batch;
+  L.H = d->n_heads;
+  L.T = d->seq_len;
+  L.sinks = sinks;
+  L.window = window;
+  L.topk = topk;
+  L.rank = rank;
+  L.cutoff = cutoff;
+  L.label = label;
+  L.boundary = boundary;
+  L.workspace = workspace;
+  L.stream = stream;
+  return hip_status(kvpop::launch_running_topk(L));
+}
+
 int kvpop_future_attn_target(const kvpop_dims* dims, const void* q, const void* k, const float* key_bias,
                              int32_t window, int32_t horizon, float* lse_ws, float* out, void* stream) {
   Sizes sz;

@@ -25,8 +25,24 @@ struct Launch {
   void* stream;        // hipStream_t
 };
 
+// Running top-k ranking (kvpop_topk.hip). All sizes already validated.
+struct TopkLaunch {
+  const float* scores;     // fp32 [B, H, T]
+  const float* log_gamma;  // fp32 [H] or nullptr (no decay)
+  int32_t B, H, T;
+  int32_t sinks, window, topk;
+  int32_t* rank;           // [B, H, T] out
+  int32_t* cutoff;         // [B, H, T] out
+  int32_t* label;          // [B, H, T] out or nullptr
+  int32_t* boundary;       // [B, H, T] out or nullptr
+  void* workspace;         // topk_workspace_words_per_seq(T) * B * H uint32 words
+  void* stream;
+};
+
 // Each returns 0 on success or the hipError_t of a failed launch.
 int launch_row_lse(const Launch& L);
 int launch_future_mass(const Launch& L);
+int launch_running_topk(const TopkLaunch& L);
+size_t topk_workspace_words_per_seq(int T);
 
 }  // namespace kvpop

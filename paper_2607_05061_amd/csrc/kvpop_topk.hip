@@ -1,0 +1,308 @@
+// gfx950 kernels for KVpop's running top-k ranking (App. B.3, App. C.2, Sec. 3.1
+// eqs. eligible_set and teacher_label).
+//
+// Per (batch row, KV head) sequence of scores r_t:
+//   * static priority (eq. static_priority_app, decay step 1), in float32:
+//       prio_t = fl(r_t - fl(t * log_gamma));
+//   * rank_t = position of t in descending priority order, ties to the earlier t;
+//   * running cutoff: at query q the eligible set is E(q) = {t : s <= t <= q - w};
+//     cutoff_q = the k-th smallest rank in E(q) once |E(q)| >= k, else T (all kept);
+//   * teacher label of t_new = q - w (+1 kept, -1 dropped, 0 if E(q) is empty) and
+//     the boundary token (the kept eligible token with the largest rank).
+//
+// The paper scans q with a Fenwick tree, one dependent tree walk per query. Here
+// every query is answered independently: E(q) is a prefix of the positions s, s+1,
+// ..., so cutoff_q is the k-th smallest value of a prefix of the array
+// A_i = rank_{s+i}, which a wavelet matrix over A answers in ceil(log2 T) constant-
+// time steps. One workgroup per sequence builds the ranks (a stable LSD radix sort
+// of 32-bit priority keys, one bit per pass) and the wavelet matrix (one stable
+// partition per bit level, most significant first); then one thread per query
+// walks the levels.
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kvpop_internal.h"
+
+namespace kvpop {
+namespace {
+
+constexpr int kPrepThreads = 1024;
+constexpr int kPrepWaves = kPrepThreads / 64;
+
+// Monotone map from float to uint32 such that larger floats give larger keys;
+// inverted so that an ascending sort puts the highest priority first. -0.0 and
+// +0.0 compare equal as numbers, so both map to the key of +0.0.
+__device__ __forceinline__ uint32_t desc_key(float f) {
+  uint32_t u = __float_as_uint(f);
+  if (u == 0x80000000u) u = 0u;
+  const uint32_t asc = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ~asc;
+}
+
+// fl(r - fl(t * lg)): two roundings, never fused into one fma, so that the ranking
+// decided by these values is reproducible from their float32 definition.
+__device__ __forceinline__ float static_priority(float r, float t, float lg) {
+#pragma clang fp contract(off)
+  const float d = t * lg;
+  return r - d;
+}
+
+// Exclusive scan (sum or max) over the 1024 threads of the block. `sh` needs
+// kPrepWaves + 1 ints. Returns the exclusive prefix; `total` gets the reduction.
+template <bool MAX>
+__device__ __forceinline__ int block_scan(int v, int* sh, int& total) {
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  int x = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(x, off);
+    if (lane >= off) x = MAX ? max(x, y) : x + y;
+  }
+  if (lane == 63) sh[wid] = x;
+  __syncthreads();
+  if (wid == 0) {
+    int s = lane < kPrepWaves ? sh[lane] : (MAX ? INT32_MIN : 0);
+    int incl = s;
+#pragma unroll
+    for (int off = 1; off < kPrepWaves; off <<= 1) {
+      const int y = __shfl_up(incl, off);
+      if (lane >= off) incl = MAX ? max(incl, y) : incl + y;
+    }
+    if (lane < kPrepWaves) sh[lane] = incl;
+  }
+  __syncthreads();
+  const int before_wave = wid > 0 ? sh[wid - 1] : (MAX ? INT32_MIN : 0);
+  const int prev = __shfl_up(x, 1);  // inclusive value of lane - 1 (all lanes take part)
+  const int excl = MAX ? (lane > 0 ? max(before_wave, prev) : before_wave) : before_wave + x - v;
+  total = sh[kPrepWaves - 1];
+  __syncthreads();
+  return excl;
+}
+
+// Stable partition of n (key, val) pairs by bit `bit` of the key: zeros first.
+// Thread t owns the contiguous chunk [t * C, t * C + C). Returns the number of zeros.
+__device__ __forceinline__ int partition_by_bit(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin,
+                                                uint32_t* __restrict__ kout, uint32_t* __restrict__ vout, int n,
+                                                int C, int bit, int* sh) {
+  const int lo = threadIdx.x * C, hi = min(n, lo + C);
+  int zeros = 0;
+  for (int i = lo; i < hi; ++i) zeros += ((kin[i] >> bit) & 1u) == 0u;
+  int ztotal;
+  int zpos = block_scan<false>(zeros, sh, ztotal);
+  int opos = ztotal + (lo - zpos);
+  for (int i = lo; i < hi; ++i) {
+    const uint32_t k = kin[i];
+    const uint32_t v = vout ? vin[i] : 0u;
+    const int dst = ((k >> bit) & 1u) ? opos++ : zpos++;
+    kout[dst] = k;
+    if (vout) vout[dst] = v;
+  }
+  __syncthreads();
+  return ztotal;
+}
+
+struct SegWork {
+  uint32_t* ka;
+  uint32_t* kb;
+  uint32_t* va;
+  uint32_t* vb;
+  int32_t* ps;     // positions in rank order
+  int32_t* pmax;   // prefix maximum of A
+  uint32_t* bits;  // [L][W + 1] bit words of each level
+  uint32_t* cnt;   // [L][W + 1] ones before each word
+  uint32_t* zeros; // [L]
+};
+
+__device__ __forceinline__ SegWork seg_work(void* ws, size_t per_seg_words, int seg, int T, int L) {
+  uint32_t* base = reinterpret_cast<uint32_t*>(ws) + (size_t)seg * per_seg_words;
+  const size_t W1 = (size_t)(T + 31) / 32 + 1;
+  SegWork s;
+  s.ka = base;
+  s.kb = s.ka + T;
+  s.va = s.kb + T;
+  s.vb = s.va + T;
+  s.ps = reinterpret_cast<int32_t*>(s.vb + T);
+  s.pmax = s.ps + T;
+  s.bits = reinterpret_cast<uint32_t*>(s.pmax + T);
+  s.cnt = s.bits + (size_t)L * W1;
+  s.zeros = s.cnt + (size_t)L * W1;
+  return s;
+}
+
+// One workgroup per sequence: priorities, ranks, sorted positions, prefix maxima
+// and the wavelet matrix over A_i = rank_{s+i}.
+__global__ __launch_bounds__(kPrepThreads) void topk_prepare_kernel(const float* __restrict__ scores,
+                                                                    const float* __restrict__ log_gamma, int H,
+                                                                    int T, int s, int L, void* ws,
+                                                                    size_t per_seg_words, int32_t* __restrict__ rank) {
+  __shared__ int sh[kPrepWaves + 1];
+  const int seg = blockIdx.x;
+  const int h = seg % H;
+  SegWork w = seg_work(ws, per_seg_words, seg, T, L);
+  const float lg = log_gamma ? log_gamma[h] : 0.f;
+  const float* r = scores + (size_t)seg * T;
+  int32_t* rk = rank + (size_t)seg * T;
+  int32_t* ps = w.ps;
+
+  // Keys and positions; no fma contraction, to match fl(r - fl(t * lg)).
+  for (int t = threadIdx.x; t < T; t += kPrepThreads) {
+    const float prio = static_priority(r[t], (float)t, lg);
+    w.ka[t] = desc_key(prio);
+    w.va[t] = (uint32_t)t;
+  }
+  __syncthreads();
+
+  // Stable LSD radix sort, one bit per pass: equal keys keep position order.
+  const int C = (T + kPrepThreads - 1) / kPrepThreads;
+  uint32_t *kin = w.ka, *kout = w.kb, *vin = w.va, *vout = w.vb;
+  for (int bit = 0; bit < 32; ++bit) {
+    partition_by_bit(kin, vin, kout, vout, T, C, bit, sh);
+    uint32_t* t0 = kin; kin = kout; kout = t0;
+    t0 = vin; vin = vout; vout = t0;
+  }
+  // vin now lists positions by rank.
+  for (int i = threadIdx.x; i < T; i += kPrepThreads) {
+    const int t = (int)vin[i];
+    ps[i] = t;
+    rk[t] = i;
+  }
+  __syncthreads();
+
+  const int n = T - s;  // eligible positions s .. T-1
+  if (n <= 0) return;
+
+  // A_i = rank_{s+i}; prefix maxima for the boundary token before saturation.
+  const int Cw = 32 * ((n + 32 * kPrepThreads - 1) / (32 * kPrepThreads));  // whole words per thread
+  {
+    const int lo = threadIdx.x * Cw, hi = min(n, lo + Cw);
+    int m = INT32_MIN;
+    for (int i = lo; i < hi; ++i) {
+      const int a = rk[s + i];
+      w.ka[i] = (uint32_t)a;
+      m = max(m, a);
+    }
+    int total;
+    int run = block_scan<true>(m, sh, total);
+    for (int i = lo; i < hi; ++i) {
+      run = max(run, (int)w.ka[i]);
+      w.pmax[i] = run;
+    }
+  }
+  __syncthreads();
+
+  // Wavelet matrix: level l splits on bit L-1-l of the current array (stable).
+  const int W = (n + 31) / 32;
+  uint32_t *ain = w.ka, *aout = w.kb;
+  for (int l = 0; l < L; ++l) {
+    const int bit = L - 1 - l;
+    uint32_t* bw = w.bits + (size_t)l * (W + 1);
+    uint32_t* cw = w.cnt + (size_t)l * (W + 1);
+    const int lo = threadIdx.x * Cw, hi = min(n, lo + Cw);
+    int ones = 0;
+    for (int i = lo; i < hi; ++i) ones += (ain[i] >> bit) & 1u;
+    int total_ones;
+    int before = block_scan<false>(ones, sh, total_ones);
+    for (int wd = lo / 32; wd * 32 < hi; ++wd) {
+      uint32_t word = 0;
+      for (int j = 0; j < 32 && wd * 32 + j < hi; ++j) word |= ((ain[wd * 32 + j] >> bit) & 1u) << j;
+      bw[wd] = word;
+      cw[wd] = (uint32_t)before;
+      before += __popc(word);
+    }
+    if (threadIdx.x == 0) {
+      bw[W] = 0u;
+      cw[W] = (uint32_t)total_ones;
+      w.zeros[l] = (uint32_t)(n - total_ones);
+    }
+    __syncthreads();
+    partition_by_bit(ain, nullptr, aout, nullptr, n, Cw, bit, sh);
+    uint32_t* t0 = ain; ain = aout; aout = t0;
+  }
+}
+
+// Ones among the first i entries of level l.
+__device__ __forceinline__ int rank1(const uint32_t* bw, const uint32_t* cw, int i) {
+  const int wd = i >> 5, b = i & 31;
+  const uint32_t mask = b ? (0xFFFFFFFFu >> (32 - b)) : 0u;
+  return (int)cw[wd] + __popc(bw[wd] & mask);
+}
+
+// One thread per (sequence, query).
+__global__ __launch_bounds__(256) void topk_query_kernel(int nseg, int T, int s, int w_win, int k, int L, void* ws,
+                                                         size_t per_seg_words, const int32_t* __restrict__ rank,
+                                                         int32_t* __restrict__ cutoff, int32_t* __restrict__ label,
+                                                         int32_t* __restrict__ boundary) {
+  const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gid >= (long long)nseg * T) return;
+  const int seg = (int)(gid / T), q = (int)(gid - (long long)seg * T);
+  SegWork w = seg_work(ws, per_seg_words, seg, T, L);
+  const int32_t* rk = rank + (size_t)seg * T;
+  const int32_t* ps = w.ps;
+  const long long tnew = (long long)q - w_win;
+  const long long p = tnew - s + 1;  // |E(q)|
+  int cut = T, lab = 0, bnd = -1;
+  if (p >= 1) {
+    if (p >= k) {
+      // k-th smallest of A[0, p) by walking the wavelet levels.
+      const int n = T - s;
+      const int W1 = (n + 31) / 32 + 1;
+      int lo = 0, hi = (int)p, kk = k, val = 0;
+      for (int l = 0; l < L; ++l) {
+        const uint32_t* bw = w.bits + (size_t)l * W1;
+        const uint32_t* cw = w.cnt + (size_t)l * W1;
+        const int o_lo = rank1(bw, cw, lo), o_hi = rank1(bw, cw, hi);
+        const int z = (hi - o_hi) - (lo - o_lo);
+        if (kk <= z) {
+          lo -= o_lo;
+          hi -= o_hi;
+        } else {
+          kk -= z;
+          const int Z = (int)w.zeros[l];
+          lo = Z + o_lo;
+          hi = Z + o_hi;
+          val |= 1 << (L - 1 - l);
+        }
+      }
+      cut = val;
+      bnd = ps[cut];
+    } else {
+      bnd = ps[w.pmax[p - 1]];
+    }
+    lab = rk[tnew] <= cut ? 1 : -1;
+  }
+  cutoff[gid] = cut;
+  if (label) label[gid] = lab;
+  if (boundary) boundary[gid] = bnd;
+}
+
+}  // namespace
+
+int topk_levels(int T) {
+  int L = 1;
+  while ((1 << L) < T) ++L;
+  return L;
+}
+
+size_t topk_workspace_words_per_seq(int T) {
+  const int L = topk_levels(T);
+  const size_t W1 = (size_t)(T + 31) / 32 + 1;
+  return 6 * (size_t)T + 2 * (size_t)L * W1 + (size_t)L + 4;
+}
+
+int launch_running_topk(const TopkLaunch& L) {
+  const int nseg = L.B * L.H;
+  const int levels = topk_levels(L.T);
+  const size_t per = topk_workspace_words_per_seq(L.T);
+  hipLaunchKernelGGL(topk_prepare_kernel, dim3(nseg), dim3(kPrepThreads), 0, (hipStream_t)L.stream, L.scores,
+                     L.log_gamma, L.H, L.T, L.sinks, levels, L.workspace, per, L.rank);
+  int e = (int)hipGetLastError();
+  if (e) return e;
+  const long long total = (long long)nseg * L.T;
+  const unsigned blocks = (unsigned)((total + 255) / 256);
+  hipLaunchKernelGGL(topk_query_kernel, dim3(blocks), dim3(256), 0, (hipStream_t)L.stream, nseg, L.T, L.sinks,
+                     L.window, L.topk, levels, L.workspace, per, L.rank, L.cutoff, L.label, L.boundary);
+  return (int)hipGetLastError();
+}
+
+}  // namespace kvpop

@@ -25,7 +25,8 @@ def _declared_functions():
 def test_header_declares_the_entry_points():
     names = set(_declared_functions())
     assert names == {"kvpop_row_lse", "kvpop_future_attn_from_lse", "kvpop_future_attn_target",
-                     "kvpop_future_attn_scores", "kvpop_strerror", "kvpop_abi_version"}
+                     "kvpop_future_attn_scores", "kvpop_running_topk", "kvpop_running_topk_workspace_size",
+                     "kvpop_strerror", "kvpop_abi_version"}
 
 
 def test_library_exports_every_declared_symbol():
@@ -148,3 +149,41 @@ def test_python_binding_rejects_cpu_tensors():
     q = torch.zeros(1, 1, 4, 64, dtype=torch.bfloat16)
     with pytest.raises(ValueError):
         kv.kvpop_row_lse(q, q, 0.125)
+
+
+def _tk(dims=(2, 3, 100), scores=A, lg=None, s=4, w=8, k=5, rank=B_, cut=C_, lab=None, bnd=None, ws=E_,
+        wsb=None):
+    d = kv.KvpopTopkDims(*dims) if dims is not None else None
+    if wsb is None:
+        wsb = kv.kvpop_running_topk_workspace_size(*dims) if dims is not None else 0
+    return kv.lib().kvpop_running_topk(ctypes.byref(d) if d is not None else None, scores, lg, s, w, k, rank, cut,
+                                       lab, bnd, ws, wsb, None)
+
+
+def test_running_topk_workspace_size():
+    assert kv.kvpop_running_topk_workspace_size(0, 1, 10) == 0
+    assert kv.kvpop_running_topk_workspace_size(1, 1, (1 << 24) + 1) == 0
+    a = kv.kvpop_running_topk_workspace_size(1, 1, 1000)
+    b = kv.kvpop_running_topk_workspace_size(2, 3, 1000)
+    assert a > 0 and b == 6 * a and a % 4 == 0
+
+
+def test_running_topk_argument_checks():
+    assert _tk(dims=None) == EINVAL
+    for dims in [(0, 1, 10), (1, 0, 10), (1, 1, 0)]:
+        assert _tk(dims=dims, wsb=1 << 20) == EINVAL
+    assert _tk(dims=(1, 1, (1 << 24) + 1), wsb=1 << 40) == EUNS
+    assert _tk(s=-1) == EINVAL
+    assert _tk(w=-1) == EINVAL
+    assert _tk(k=0) == EINVAL
+    assert _tk(scores=None) == EINVAL
+    assert _tk(rank=None) == EINVAL
+    assert _tk(cut=None) == EINVAL
+    assert _tk(ws=None) == EINVAL
+    need = kv.kvpop_running_topk_workspace_size(2, 3, 100)
+    assert _tk(wsb=need - 1) == EINVAL
+    assert _tk(scores=A + 4) == EUNS
+    assert _tk(lab=D_ + 8) == EUNS
+    assert _tk(cut=B_ + 16) == EINVAL                 # rank and cutoff overlap
+    assert _tk(lab=A + 16) == EINVAL                  # label over the scores
+    assert _tk(ws=C_ - 64) == EINVAL                  # workspace over the cutoff

@@ -137,3 +137,17 @@ def test_f32_priority_rounding_is_per_operation():
     p = oracle.static_priority_f32(r, -1e-3)
     want = [np.float32(1.0) - np.float32(np.float32(t) * np.float32(-1e-3)) for t in range(3)]
     np.testing.assert_array_equal(p, np.array(want, dtype=np.float32))
+
+
+def test_teacher_labels_query_subset_matches_full():
+    rng = np.random.default_rng(11)
+    T, s, w, k = 120, 2, 5, 9
+    rank = oracle.ranks_from_priority(rng.standard_normal(T))
+    tau = oracle.running_cutoff_bruteforce(rank, s, w, k)
+    y, tb = oracle.teacher_labels(rank, tau, s, w)
+    qs = [0, 6, 7, 30, 119]
+    ys, tbs = oracle.teacher_labels(rank, tau, s, w, queries=qs)
+    np.testing.assert_array_equal(ys[qs], y[qs])
+    np.testing.assert_array_equal(tbs[qs], tb[qs])
+    rest = np.setdiff1d(np.arange(T), qs)
+    assert np.all(ys[rest] == 0) and np.all(tbs[rest] == -1)
