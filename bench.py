@@ -29,6 +29,7 @@ METRIC = "key-query pairs/sec and MFMA util (% bf16 peak), Qwen3-8B-shaped layer
 PEAK_BF16_TFLOPS = 2516.6  # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 flop/clk/CU
 KERNEL_SRC = os.path.join(ROOT, "paper_2607_05061_amd", "csrc", "kvpop_kernels.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+TOPK_BUDGET = (4, 256, 2016)  # sinks s, protected window w, top-k k: the paper's fixed budget B = s + w + k = 2276
 
 
 def log(*a):
@@ -264,6 +265,27 @@ def main():
            "ms_per_step": round(evs2[0][0].elapsed_time(evs2[-1][-1]) / n_epi, 4),
            "pass2_with_epilogue_ms": round(float(np.mean([e[1].elapsed_time(e[2]) for e in evs2])), 4)}
 
+    # Running top-k on the live target (App. B.3, App. C): ranks, cutoffs, teacher labels
+    # and boundary tokens per (batch, KV head), with the paper's fixed budget and a
+    # per-head decay in the learned range.
+    s_, w_, k_ = TOPK_BUDGET
+    lg = torch.tensor(np.log(np.linspace(0.999, 0.999999, w.Hkv)), dtype=torch.float32, device=dev)
+    ws = torch.empty(kv.kvpop_running_topk_workspace_size(w.B, w.Hkv, w.T), dtype=torch.uint8, device=dev)
+    for _ in range(2):
+        kv.kvpop_running_topk(scores, s_, w_, k_, log_gamma=lg, workspace=ws)
+    n_tk = max(1, args.steps // 2)
+    ev_tk = [torch.cuda.Event(enable_timing=True) for _ in range(n_tk + 1)]
+    ev_tk[0].record()
+    for i in range(n_tk):
+        tk = kv.kvpop_running_topk(scores, s_, w_, k_, log_gamma=lg, workspace=ws)
+        ev_tk[i + 1].record()
+    torch.cuda.synchronize()
+    tk_ms = ev_tk[0].elapsed_time(ev_tk[-1]) / n_tk
+    assert bool((torch.sort(tk["rank"], dim=-1).values == torch.arange(w.T, device=dev, dtype=torch.int32)).all()), \
+        "ranks are not a permutation"
+    topk = {"budget": {"sinks": s_, "window": w_, "k": k_}, "steps": n_tk, "ms": round(tk_ms, 4),
+            "tokens_per_s": w.B * w.Hkv * w.T / (tk_ms * 1e-3)}
+
     # Parity sanity on the live result: full-future masses of a head sum to T.
     for i, (a, b) in enumerate(w.bands):
         if a == 0 and b < 0:
@@ -297,6 +319,7 @@ def main():
         "wall_s": round(wall, 3),
         "roofline": roofline,
         "target_epilogue": epi,
+        "running_topk": topk,
         "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)
