@@ -20,6 +20,10 @@ The running top-k policy pieces (static priorities, ranks, cutoffs, the sparse
 mask and the sparse log-normaliser of App. C and App. D.3) are in
 ``oracle.running_topk``.
 
+The running top-k sparse attention forward (App. C.1, C.3) with its sparse LSE,
+and the token lifetimes [t, e_t) that the running mask reduces to, are in
+``oracle.sparse_attention``.
+
 The target epilogue of App. D.4 step 5 (aggregation over the G query heads and
 count normalisation, App. B.1-B.2) is in ``oracle.target``.
 
@@ -47,4 +51,11 @@ from .running_topk import (  # noqa: F401
     static_priority,
     static_priority_f32,
     teacher_labels,
+)
+from .sparse_attention import (  # noqa: F401
+    eviction_times,
+    eviction_times_bruteforce,
+    lifetime_mask,
+    running_topk_mask_rows,
+    sparse_attention,
 )
