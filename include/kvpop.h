@@ -60,7 +60,7 @@
 extern "C" {
 #endif
 
-#define KVPOP_ABI_VERSION 1
+#define KVPOP_ABI_VERSION 2
 
 /* Status codes returned by every entry point. */
 enum {
@@ -154,6 +154,13 @@ int kvpop_future_attn_scores(const kvpop_dims* dims, const void* q, const void* 
  *              empty (eq. teacher_label)
  *   boundary_q = the retained token of E(q) with the largest rank (the teacher's
  *              cutoff token t_bnd), -1 if E(q) is empty
+ *   evict_t  = the first query q >= t that no longer keeps token t under the mask
+ *              of App. C.1 eq. running_topk_mask_app, T if every later query keeps
+ *              it. The cutoff never increases with q (before saturation it is T;
+ *              after, the k-th smallest rank of a growing set), so a dropped token
+ *              never returns and that mask is exactly  t <= q < evict_t:
+ *              evict_t = T for t < sinks, else
+ *              min(T, max(t + window, first q with cutoff_q < rank_t)).
  * --------------------------------------------------------------------------- */
 typedef struct kvpop_topk_dims {
   int32_t batch;    /* B >= 1 */
@@ -166,13 +173,13 @@ typedef struct kvpop_topk_dims {
 size_t kvpop_running_topk_workspace_size(const kvpop_topk_dims* dims);
 
 /* scores: fp32 [B,H,T]; log_gamma: fp32 [H] or NULL; sinks >= 0, window >= 0,
- * topk >= 1. Outputs int32 [B,H,T]: rank and cutoff (required), label and boundary
- * (optional, NULL to skip). workspace: caller-allocated device memory of at least
+ * topk >= 1. Outputs int32 [B,H,T]: rank and cutoff (required), label, boundary and
+ * evict (optional, NULL to skip). workspace: caller-allocated device memory of at least
  * kvpop_running_topk_workspace_size bytes, 16-byte aligned; its contents on entry
  * do not matter. All outputs are fully overwritten. */
 int kvpop_running_topk(const kvpop_topk_dims* dims, const float* scores, const float* log_gamma, int32_t sinks,
                        int32_t window, int32_t topk, int32_t* rank, int32_t* cutoff, int32_t* label,
-                       int32_t* boundary, void* workspace, size_t workspace_bytes, void* stream);
+                       int32_t* boundary, int32_t* evict, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Human-readable text for a status code. For KVPOP_EHIP it is the HIP runtime's
  * message for the last failure on the calling thread. Never returns NULL; the

@@ -33,7 +33,7 @@ KVPOP_EUNSUPPORTED = 2
 KVPOP_EHIP = 3
 KVPOP_AGG_MAX = 0
 KVPOP_AGG_MEAN = 1
-ABI_VERSION = 1
+ABI_VERSION = 2
 
 _PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 _LIB: Optional[ctypes.CDLL] = None
@@ -87,7 +87,7 @@ def lib() -> ctypes.CDLL:
         L.kvpop_future_attn_scores.restype = ctypes.c_int
         L.kvpop_running_topk_workspace_size.argtypes = [ctypes.POINTER(KvpopTopkDims)]
         L.kvpop_running_topk_workspace_size.restype = ctypes.c_size_t
-        L.kvpop_running_topk.argtypes = [ctypes.POINTER(KvpopTopkDims), P, P, I32, I32, I32, P, P, P, P, P,
+        L.kvpop_running_topk.argtypes = [ctypes.POINTER(KvpopTopkDims), P, P, I32, I32, I32, P, P, P, P, P, P,
                                          ctypes.c_size_t, P]
         L.kvpop_running_topk.restype = ctypes.c_int
         L.kvpop_strerror.argtypes = [ctypes.c_int]
@@ -240,9 +240,10 @@ def kvpop_running_topk_workspace_size(batch: int, n_heads: int, seq_len: int) ->
 
 
 def kvpop_running_topk(scores, sinks: int, window: int, topk: int, log_gamma=None, labels: bool = True,
-                       workspace=None, stream=None):
-    """Ranks, running cutoffs and (optionally) teacher labels and boundary tokens for
-    scores [B, H, T] (App. B.3, App. C). Returns a dict of int32 tensors."""
+                       evict: bool = False, workspace=None, stream=None):
+    """Ranks, running cutoffs and (optionally) teacher labels and boundary tokens, and
+    token eviction queries, for scores [B, H, T] (App. B.3, App. C). Returns a dict of
+    int32 tensors."""
     torch = _torch()
     _check_tensor(scores, "scores", torch.float32, None)
     if scores.dim() != 3:
@@ -263,12 +264,15 @@ def kvpop_running_topk(scores, sinks: int, window: int, topk: int, log_gamma=Non
     if labels:
         out["label"] = torch.empty((B, H, T), dtype=torch.int32, device=scores.device)
         out["boundary"] = torch.empty((B, H, T), dtype=torch.int32, device=scores.device)
+    if evict:
+        out["evict"] = torch.empty((B, H, T), dtype=torch.int32, device=scores.device)
     d = KvpopTopkDims(B, H, T)
     st = lib().kvpop_running_topk(ctypes.byref(d), scores.data_ptr(),
                                   log_gamma.data_ptr() if log_gamma is not None else None, int(sinks), int(window),
                                   int(topk), out["rank"].data_ptr(), out["cutoff"].data_ptr(),
                                   out["label"].data_ptr() if labels else None,
-                                  out["boundary"].data_ptr() if labels else None, workspace.data_ptr(),
+                                  out["boundary"].data_ptr() if labels else None,
+                                  out["evict"].data_ptr() if evict else None, workspace.data_ptr(),
                                   workspace.numel() * workspace.element_size(), _stream_ptr(stream, scores.device))
     if st != KVPOP_OK:
         raise KvpopError(st, "kvpop_running_topk")

@@ -195,27 +195,27 @@ size_t kvpop_running_topk_workspace_size(const kvpop_topk_dims* d) {
 
 int kvpop_running_topk(const kvpop_topk_dims* d, const float* scores, const float* log_gamma, int32_t sinks,
                        int32_t window, int32_t topk, int32_t* rank, int32_t* cutoff, int32_t* label,
-                       int32_t* boundary, void* workspace, size_t workspace_bytes, void* stream) {
+                       int32_t* boundary, int32_t* evict, void* workspace, size_t workspace_bytes, void* stream) {
   if (!d || d->batch < 1 || d->n_heads < 1 || d->seq_len < 1) return KVPOP_EINVAL;
   if (d->seq_len > KVPOP_MAX_SEQ_LEN) return KVPOP_EUNSUPPORTED;
   if (sinks < 0 || window < 0 || topk < 1) return KVPOP_EINVAL;
   if (!scores || !rank || !cutoff || !workspace) return KVPOP_EINVAL;
   const size_t need = kvpop_running_topk_workspace_size(d);
   if (need == 0 || workspace_bytes < need) return KVPOP_EINVAL;
-  const void* ptrs[] = {scores, log_gamma, rank, cutoff, label, boundary, workspace};
+  const void* ptrs[] = {scores, log_gamma, rank, cutoff, label, boundary, evict, workspace};
   for (const void* p : ptrs)
     if (p && !aligned16(p)) return KVPOP_EUNSUPPORTED;
   const int64_t n = (int64_t)d->batch * d->n_heads * d->seq_len;
   if (n / d->seq_len / d->n_heads != d->batch || n * 4 > INT64_MAX / 2) return KVPOP_EINVAL;
   const int64_t b = n * 4;
   // Outputs must not overlap each other, the inputs or the workspace.
-  const void* outs[] = {rank, cutoff, label, boundary};
-  for (int i = 0; i < 4; ++i) {
+  const void* outs[] = {rank, cutoff, label, boundary, evict};
+  for (int i = 0; i < 5; ++i) {
     if (!outs[i]) continue;
     if (overlap(outs[i], b, scores, b) || overlap(outs[i], b, log_gamma, (int64_t)d->n_heads * 4) ||
         overlap(outs[i], b, workspace, (int64_t)need))
       return KVPOP_EINVAL;
-    for (int j = i + 1; j < 4; ++j)
+    for (int j = i + 1; j < 5; ++j)
       if (overlap(outs[i], b, outs[j], b)) return KVPOP_EINVAL;
   }
   if (overlap(workspace, (int64_t)need, scores, b) || overlap(workspace, (int64_t)need, log_gamma, (int64_t)d->n_heads * 4))
@@ -233,6 +233,7 @@ int kvpop_running_topk(const kvpop_topk_dims* d, const float* scores, const floa
   L.cutoff = cutoff;
   L.label = label;
   L.boundary = boundary;
+  L.evict = evict;
   L.workspace = workspace;
   L.stream = stream;
   return hip_status(kvpop::launch_running_topk(L));

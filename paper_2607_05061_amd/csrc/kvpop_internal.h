@@ -35,6 +35,7 @@ struct TopkLaunch {
   int32_t* cutoff;         // [B, H, T] out
   int32_t* label;          // [B, H, T] out or nullptr
   int32_t* boundary;       // [B, H, T] out or nullptr
+  int32_t* evict;          // [B, H, T] out or nullptr
   void* workspace;         // topk_workspace_words_per_seq(T) * B * H uint32 words
   void* stream;
 };

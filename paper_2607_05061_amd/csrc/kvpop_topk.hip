@@ -276,6 +276,32 @@ __global__ __launch_bounds__(256) void topk_query_kernel(int nseg, int T, int s,
   if (boundary) boundary[gid] = bnd;
 }
 
+// One thread per (sequence, token): the query at which the token leaves the mask.
+// cutoff is non-increasing in q, so the first q with cutoff_q < rank_t is found by
+// binary search.
+__global__ __launch_bounds__(256) void topk_evict_kernel(int nseg, int T, int s, int w_win,
+                                                         const int32_t* __restrict__ rank,
+                                                         const int32_t* __restrict__ cutoff,
+                                                         int32_t* __restrict__ evict) {
+  const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gid >= (long long)nseg * T) return;
+  const int seg = (int)(gid / T), t = (int)(gid - (long long)seg * T);
+  int e = T;
+  if (t >= s) {
+    const int32_t* cut = cutoff + (size_t)seg * T;
+    const int r = rank[gid];
+    int lo = 0, hi = T;  // first q in [lo, hi) with cut[q] < r, or T
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (cut[mid] < r) hi = mid;
+      else lo = mid + 1;
+    }
+    const long long leave = (long long)t + w_win;
+    e = (int)(lo > leave ? lo : (leave < T ? leave : T));
+  }
+  evict[gid] = e;
+}
+
 }  // namespace
 
 int topk_levels(int T) {
@@ -302,6 +328,10 @@ int launch_running_topk(const TopkLaunch& L) {
   const unsigned blocks = (unsigned)((total + 255) / 256);
   hipLaunchKernelGGL(topk_query_kernel, dim3(blocks), dim3(256), 0, (hipStream_t)L.stream, nseg, L.T, L.sinks,
                      L.window, L.topk, levels, L.workspace, per, L.rank, L.cutoff, L.label, L.boundary);
+  e = (int)hipGetLastError();
+  if (e || !L.evict) return e;
+  hipLaunchKernelGGL(topk_evict_kernel, dim3(blocks), dim3(256), 0, (hipStream_t)L.stream, nseg, L.T, L.sinks,
+                     L.window, L.rank, L.cutoff, L.evict);
   return (int)hipGetLastError();
 }
 

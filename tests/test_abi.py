@@ -37,7 +37,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version_and_strerror():
-    assert kv.kvpop_abi_version() == 1
+    assert kv.kvpop_abi_version() == kv.ABI_VERSION == 2
     texts = {c: kv.kvpop_strerror(c) for c in (kv.KVPOP_OK, kv.KVPOP_EINVAL, kv.KVPOP_EUNSUPPORTED, kv.KVPOP_EHIP, 99)}
     assert texts[kv.KVPOP_OK] == "success"
     assert "invalid" in texts[kv.KVPOP_EINVAL]
@@ -151,13 +151,13 @@ def test_python_binding_rejects_cpu_tensors():
         kv.kvpop_row_lse(q, q, 0.125)
 
 
-def _tk(dims=(2, 3, 100), scores=A, lg=None, s=4, w=8, k=5, rank=B_, cut=C_, lab=None, bnd=None, ws=E_,
+def _tk(dims=(2, 3, 100), scores=A, lg=None, s=4, w=8, k=5, rank=B_, cut=C_, lab=None, bnd=None, ev=None, ws=E_,
         wsb=None):
     d = kv.KvpopTopkDims(*dims) if dims is not None else None
     if wsb is None:
         wsb = kv.kvpop_running_topk_workspace_size(*dims) if dims is not None else 0
     return kv.lib().kvpop_running_topk(ctypes.byref(d) if d is not None else None, scores, lg, s, w, k, rank, cut,
-                                       lab, bnd, ws, wsb, None)
+                                       lab, bnd, ev, ws, wsb, None)
 
 
 def test_running_topk_workspace_size():
@@ -187,3 +187,5 @@ def test_running_topk_argument_checks():
     assert _tk(cut=B_ + 16) == EINVAL                 # rank and cutoff overlap
     assert _tk(lab=A + 16) == EINVAL                  # label over the scores
     assert _tk(ws=C_ - 64) == EINVAL                  # workspace over the cutoff
+    assert _tk(ev=D_ + 4) == EUNS                     # misaligned eviction output
+    assert _tk(ev=C_ + 16) == EINVAL                  # eviction output over the cutoff

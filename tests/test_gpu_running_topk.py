@@ -17,7 +17,7 @@ pytestmark = pytest.mark.gpu
 
 def _expected(scores, log_gamma, s, w, k, queries=None):
     B, H, T = scores.shape
-    exp = {n: np.empty((B, H, T), dtype=np.int64) for n in ("rank", "cutoff", "label", "boundary")}
+    exp = {n: np.empty((B, H, T), dtype=np.int64) for n in ("rank", "cutoff", "label", "boundary", "evict")}
     for b in range(B):
         for h in range(H):
             lg = 0.0 if log_gamma is None else log_gamma[h]
@@ -27,13 +27,14 @@ def _expected(scores, log_gamma, s, w, k, queries=None):
             y, tb = oracle.teacher_labels(rank, tau, s, w, queries)
             exp["rank"][b, h], exp["cutoff"][b, h] = rank, tau
             exp["label"][b, h], exp["boundary"][b, h] = y, tb
+            exp["evict"][b, h] = oracle.eviction_times(rank, tau, s, w)
     return exp
 
 
-def _run(scores, log_gamma, s, w, k, labels=True):
+def _run(scores, log_gamma, s, w, k, labels=True, evict=True):
     sc = torch.from_numpy(scores).to("cuda")
     lg = torch.from_numpy(np.asarray(log_gamma, dtype=np.float32)).to("cuda") if log_gamma is not None else None
-    out = kv.kvpop_running_topk(sc, s, w, k, log_gamma=lg, labels=labels)
+    out = kv.kvpop_running_topk(sc, s, w, k, log_gamma=lg, labels=labels, evict=evict)
     torch.cuda.synchronize()
     return {n: v.cpu().numpy().astype(np.int64) for n, v in out.items()}
 
@@ -45,6 +46,7 @@ def test_hand_case():
     np.testing.assert_array_equal(got["cutoff"][0, 0], [5, 5, 5, 3, 3])
     np.testing.assert_array_equal(got["label"][0, 0], [0, 0, 1, 1, -1])
     np.testing.assert_array_equal(got["boundary"][0, 0], [-1, -1, 1, 1, 1])
+    np.testing.assert_array_equal(got["evict"][0, 0], [5, 5, 5, 4, 5])
 
 
 CASES = [
@@ -70,7 +72,7 @@ def test_matches_oracle(case, decay):
     log_gamma = np.log(rng.uniform(0.99, 0.9999, size=H)).astype(np.float32) if decay else None
     got = _run(scores, log_gamma, s, w, k)
     exp = _expected(scores, log_gamma, s, w, k)
-    for n in ("rank", "cutoff", "label", "boundary"):
+    for n in ("rank", "cutoff", "label", "boundary", "evict"):
         np.testing.assert_array_equal(got[n], exp[n], err_msg=n)
 
 
@@ -79,13 +81,13 @@ def test_ties_break_to_earlier_position():
     scores = (np.round(rng.standard_normal((2, 2, 700)) * 2) / 2).astype(np.float32)  # many exact ties
     got = _run(scores, None, 2, 8, 40)
     exp = _expected(scores, None, 2, 8, 40)
-    for n in ("rank", "cutoff", "label", "boundary"):
+    for n in ("rank", "cutoff", "label", "boundary", "evict"):
         np.testing.assert_array_equal(got[n], exp[n], err_msg=n)
 
 
 def test_labels_optional():
     scores = np.random.default_rng(4).standard_normal((1, 2, 200)).astype(np.float32)
-    got = _run(scores, None, 1, 4, 10, labels=False)
+    got = _run(scores, None, 1, 4, 10, labels=False, evict=False)
     assert set(got) == {"rank", "cutoff"}
     exp = _expected(scores, None, 1, 4, 10)
     np.testing.assert_array_equal(got["cutoff"], exp["cutoff"])
@@ -105,6 +107,7 @@ def test_paper_budget_at_benchmark_size():
         e = _expected(scores[b:b + 1, h:h + 1], log_gamma[h:h + 1], s, w, k, queries=qs)
         np.testing.assert_array_equal(got["rank"][b, h], e["rank"][0, 0])
         np.testing.assert_array_equal(got["cutoff"][b, h], e["cutoff"][0, 0])
+        np.testing.assert_array_equal(got["evict"][b, h], e["evict"][0, 0])
         np.testing.assert_array_equal(got["label"][b, h, qs], e["label"][0, 0, qs])
         np.testing.assert_array_equal(got["boundary"][b, h, qs], e["boundary"][0, 0, qs])
     # every sequence: ranks are a permutation, cutoffs monotone once saturated
