@@ -186,6 +186,31 @@ int kvpop_running_topk(const kvpop_topk_dims* dims, const float* scores, const f
  * string stays valid until the next library call on the same thread. */
 const char* kvpop_strerror(int status);
 
+/* ---------------------------------------------------------------------------
+ * Running top-k sparse attention forward (Sec. 3.2; App. C.1 eq.
+ * running_topk_mask_app; App. C.3): the student's attention over the keys that
+ * its fixed-budget mask keeps, returning the output and the sparse LSE that the
+ * target pass consumes (Sec. 3.2 eq. sparse_lse_main; App. D.3).
+ *
+ * Key t of KV head h is kept by query q iff  t <= q < evict[b, h, t].  With evict
+ * from kvpop_running_topk this is exactly the running top-k mask (sinks, protected
+ * window, and the eligible tokens whose rank is within the cutoff); evict = T for
+ * every key gives dense causal attention and evict[t] = t + w a sliding window.
+ * For every (b, qh, q), with h = qh / G and l(q, t) = scale <q, k_t> + key_bias[t]:
+ *   lse[b, qh, q]    = log sum_{kept t} exp l(q, t)        (natural log)
+ *   o[b, qh, q, :]   = sum_{kept t} exp(l(q, t) - lse) v[b, h, t, :]
+ * A query that keeps no key gets o = 0 and lse = -inf.
+ *
+ * q: bf16 [B,Hq,T,D]; k, v: bf16 [B,Hkv,T,D]; key_bias: fp32 [T] or NULL;
+ * evict: int32 [B,Hkv,T]; o: bf16 [B,Hq,T,D] (output); lse: fp32 [B,Hq,T] (output).
+ * The probabilities are rounded to bf16 for the product with v; the LSE uses them
+ * unrounded. Requirements beyond the common ones: Hq / Hkv a power of two and
+ * T * D * 2 < 2^31 (KVPOP_EUNSUPPORTED otherwise); outputs must not overlap any
+ * input or each other (KVPOP_EINVAL). Device pointers, 16-byte aligned; the call
+ * allocates nothing and is asynchronous on `stream`. */
+int kvpop_sparse_attn_fwd(const kvpop_dims* dims, const void* q, const void* k, const void* v,
+                          const float* key_bias, const int32_t* evict, void* o, float* lse, void* stream);
+
 /* KVPOP_ABI_VERSION of the loaded library. */
 int kvpop_abi_version(void);
 

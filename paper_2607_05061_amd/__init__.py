@@ -24,7 +24,7 @@ __all__ = [
     "KVPOP_OK", "KVPOP_EINVAL", "KVPOP_EUNSUPPORTED", "KVPOP_EHIP", "KvpopDims", "KvpopError",
     "lib", "lib_path", "kvpop_row_lse", "kvpop_future_attn_from_lse", "kvpop_future_attn_target",
     "kvpop_future_attn_scores", "kvpop_strerror", "kvpop_abi_version", "KVPOP_AGG_MAX", "KVPOP_AGG_MEAN",
-    "KvpopTopkDims", "kvpop_running_topk", "kvpop_running_topk_workspace_size",
+    "KvpopTopkDims", "kvpop_running_topk", "kvpop_running_topk_workspace_size", "kvpop_sparse_attn_fwd",
 ]
 
 KVPOP_OK = 0
@@ -90,6 +90,8 @@ def lib() -> ctypes.CDLL:
         L.kvpop_running_topk.argtypes = [ctypes.POINTER(KvpopTopkDims), P, P, I32, I32, I32, P, P, P, P, P, P,
                                          ctypes.c_size_t, P]
         L.kvpop_running_topk.restype = ctypes.c_int
+        L.kvpop_sparse_attn_fwd.argtypes = [ctypes.POINTER(KvpopDims), P, P, P, P, P, P, P, P]
+        L.kvpop_sparse_attn_fwd.restype = ctypes.c_int
         L.kvpop_strerror.argtypes = [ctypes.c_int]
         L.kvpop_strerror.restype = ctypes.c_char_p
         L.kvpop_abi_version.argtypes = []
@@ -277,3 +279,30 @@ def kvpop_running_topk(scores, sinks: int, window: int, topk: int, log_gamma=Non
     if st != KVPOP_OK:
         raise KvpopError(st, "kvpop_running_topk")
     return out
+
+
+def kvpop_sparse_attn_fwd(q, k, v, evict, scale: float, key_bias=None, o=None, lse=None, stream=None):
+    """Running top-k sparse attention forward (Sec. 3.2, App. C): key t of KV head h is
+    kept by query q iff t <= q < evict[b, h, t]. Returns (o bf16 [B, Hq, T, D],
+    lse fp32 [B, Hq, T])."""
+    torch = _torch()
+    d = _dims(q, k, scale)
+    qp, kp, bp = _prep_inputs(q, k, key_bias)
+    _check_tensor(v, "v", torch.bfloat16, q.device)
+    if tuple(v.shape) != tuple(k.shape):
+        raise ValueError("v must have the shape of k")
+    _check_tensor(evict, "evict", torch.int32, q.device)
+    if tuple(evict.shape) != (d.batch, d.n_kv_heads, d.seq_len):
+        raise ValueError("evict must be [B, Hkv, T]")
+    if o is None:
+        o = torch.empty(tuple(q.shape), dtype=torch.bfloat16, device=q.device)
+    else:
+        _check_tensor(o, "o", torch.bfloat16, q.device)
+        if tuple(o.shape) != tuple(q.shape):
+            raise ValueError("o must have the shape of q")
+    lse = _prep_out(lse, "lse", (d.batch, d.n_q_heads, d.seq_len), q.device)
+    st = lib().kvpop_sparse_attn_fwd(ctypes.byref(d), qp, kp, v.data_ptr(), bp, evict.data_ptr(), o.data_ptr(),
+                                     lse.data_ptr(), _stream_ptr(stream, q.device))
+    if st != KVPOP_OK:
+        raise KvpopError(st, "kvpop_sparse_attn_fwd")
+    return o, lse

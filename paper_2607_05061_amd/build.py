@@ -15,7 +15,7 @@ CSRC = os.path.join(PKG_DIR, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_NAME = "libkvpop.so"
 LIB_PATH = os.path.join(PKG_DIR, LIB_NAME)
-SOURCES = ["kvpop_api.cpp", "kvpop_kernels.hip", "kvpop_topk.hip"]
+SOURCES = ["kvpop_api.cpp", "kvpop_kernels.hip", "kvpop_topk.hip", "kvpop_sparse_attn.hip"]
 
 # Packed fp32 VALU forms are disabled for all device code.
 HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

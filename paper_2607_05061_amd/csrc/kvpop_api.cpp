@@ -239,6 +239,43 @@ int kvpop_running_topk(const kvpop_topk_dims* d, const float* scores, const floa
   return hip_status(kvpop::launch_running_topk(L));
 }
 
+int kvpop_sparse_attn_fwd(const kvpop_dims* dims, const void* q, const void* k, const void* v,
+                          const float* key_bias, const int32_t* evict, void* o, float* lse, void* stream) {
+  Sizes sz;
+  int st = check_inputs(dims, q, k, key_bias, &sz);
+  if (st != KVPOP_OK) return st;
+  const int G = dims->n_q_heads / dims->n_kv_heads;
+  if ((G & (G - 1)) != 0) return KVPOP_EUNSUPPORTED;
+  if ((int64_t)dims->seq_len * dims->head_dim * 2 > INT32_MAX) return KVPOP_EUNSUPPORTED;
+  if (!v || !evict) return KVPOP_EINVAL;
+  if (!aligned16(v) || !aligned16(evict)) return KVPOP_EUNSUPPORTED;
+  const int64_t ev_bytes = (int64_t)dims->batch * dims->n_kv_heads * dims->seq_len * 4;
+  // o must not overlap q, k, key_bias, lse, v or evict; lse likewise.
+  st = check_output(o, sz.q_elems * 2, sz, dims, q, k, key_bias, lse, sz.row_elems * 4);
+  if (st != KVPOP_OK) return st;
+  st = check_output(lse, sz.row_elems * 4, sz, dims, q, k, key_bias, o, sz.q_elems * 2);
+  if (st != KVPOP_OK) return st;
+  if (overlap(o, sz.q_elems * 2, v, sz.k_elems * 2) || overlap(o, sz.q_elems * 2, evict, ev_bytes) ||
+      overlap(lse, sz.row_elems * 4, v, sz.k_elems * 2) || overlap(lse, sz.row_elems * 4, evict, ev_bytes))
+    return KVPOP_EINVAL;
+  kvpop::SparseLaunch L{};
+  L.q = static_cast<const uint16_t*>(q);
+  L.k = static_cast<const uint16_t*>(k);
+  L.v = static_cast<const uint16_t*>(v);
+  L.bias = key_bias;
+  L.evict = evict;
+  L.o = static_cast<uint16_t*>(o);
+  L.lse = lse;
+  L.B = dims->batch;
+  L.Hq = dims->n_q_heads;
+  L.Hkv = dims->n_kv_heads;
+  L.T = dims->seq_len;
+  L.D = dims->head_dim;
+  L.scale = dims->scale;
+  L.stream = stream;
+  return hip_status(kvpop::launch_sparse_attn_fwd(L));
+}
+
 int kvpop_future_attn_target(const kvpop_dims* dims, const void* q, const void* k, const float* key_bias,
                              int32_t window, int32_t horizon, float* lse_ws, float* out, void* stream) {
   Sizes sz;

@@ -40,10 +40,30 @@ struct TopkLaunch {
   void* stream;
 };
 
+// Running top-k sparse attention forward (kvpop_sparse_attn.hip). All sizes
+// already validated; the plan fields are filled by sparse_attn_plan.
+struct SparseLaunch {
+  const uint16_t* q;      // bf16 [B, Hq, T, D]
+  const uint16_t* k;      // bf16 [B, Hkv, T, D]
+  const uint16_t* v;      // bf16 [B, Hkv, T, D]
+  const float* bias;      // fp32 [T] or nullptr
+  const int32_t* evict;   // int32 [B, Hkv, T]
+  uint16_t* o;            // bf16 [B, Hq, T, D] out
+  float* lse;             // fp32 [B, Hq, T] out
+  int32_t B, Hq, Hkv, T, D;
+  float scale;
+  void* stream;
+  // plan
+  int32_t G, hpw, wq, qt, hc, nch, ntiles;
+  float c;                // scale * log2(e)
+};
+void sparse_attn_plan(SparseLaunch& L);
+
 // Each returns 0 on success or the hipError_t of a failed launch.
 int launch_row_lse(const Launch& L);
 int launch_future_mass(const Launch& L);
 int launch_running_topk(const TopkLaunch& L);
+int launch_sparse_attn_fwd(SparseLaunch L);
 size_t topk_workspace_words_per_seq(int T);
 
 }  // namespace kvpop

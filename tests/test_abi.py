@@ -26,7 +26,7 @@ def test_header_declares_the_entry_points():
     names = set(_declared_functions())
     assert names == {"kvpop_row_lse", "kvpop_future_attn_from_lse", "kvpop_future_attn_target",
                      "kvpop_future_attn_scores", "kvpop_running_topk", "kvpop_running_topk_workspace_size",
-                     "kvpop_strerror", "kvpop_abi_version"}
+                     "kvpop_sparse_attn_fwd", "kvpop_strerror", "kvpop_abi_version"}
 
 
 def test_library_exports_every_declared_symbol():
@@ -189,3 +189,30 @@ def test_running_topk_argument_checks():
     assert _tk(ws=C_ - 64) == EINVAL                  # workspace over the cutoff
     assert _tk(ev=D_ + 4) == EUNS                     # misaligned eviction output
     assert _tk(ev=C_ + 16) == EINVAL                  # eviction output over the cutoff
+
+
+F_, G_ = 0x60000000, 0x70000000
+
+
+def _sa(d, q=A, k=B_, v=C_, bias=None, ev=D_, o=E_, lse=F_):
+    return kv.lib().kvpop_sparse_attn_fwd(ctypes.byref(d) if d is not None else None, q, k, v, bias, ev, o, lse,
+                                          None)
+
+
+def test_sparse_attn_argument_checks():
+    """Every call here is rejected during validation (the pointers are fake)."""
+    d = _dims()
+    assert _sa(None) == EINVAL
+    assert _sa(_dims(Hq=3, Hkv=2)) == EINVAL             # Hq % Hkv != 0
+    assert _sa(_dims(Hq=6, Hkv=2)) == EUNS               # G = 3, not a power of two
+    assert _sa(_dims(D=96)) == EUNS
+    assert _sa(_dims(T=1 << 23)) == EUNS                 # T * D * 2 >= 2^31
+    assert _sa(_dims(scale=0.0)) == EINVAL
+    for name in ("q", "k", "v", "ev", "o", "lse"):
+        assert _sa(d, **{name: None}) == EINVAL, name
+    for name in ("q", "k", "v", "ev", "o", "lse"):
+        assert _sa(d, **{name: {"q": A, "k": B_, "v": C_, "ev": D_, "o": E_, "lse": F_}[name] + 8}) == EUNS, name
+    assert _sa(d, o=A + 64) == EINVAL                    # o over q
+    assert _sa(d, lse=C_ + 16) == EINVAL                 # lse over v
+    assert _sa(d, o=D_ - 16) == EINVAL                   # o over evict
+    assert _sa(d, lse=E_ + 32) == EINVAL                 # lse over o

@@ -10,7 +10,9 @@ from .gen import (  # noqa: F401
     Workload,
     bf16_round_bits,
     make,
+    make_scores,
     make_slice,
+    make_values,
     rmsnorm,
     rope,
 )

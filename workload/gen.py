@@ -105,6 +105,7 @@ class Workload:
     k_bits: np.ndarray
     bias: Optional[np.ndarray]
     bands: list = field(default_factory=list)
+    seed: int = 0
 
     @property
     def G(self) -> int:
@@ -204,4 +205,25 @@ def make(name_or_cfg, T: Optional[int] = None, B: Optional[int] = None, threads:
         bias[0] = 3.0
     scale = float(np.float32(cfg["scale"]))
     return Workload(name=name, B=Bn, Hq=Hq, Hkv=Hkv, T=T, D=D, scale=scale, q_bits=q_bits,
-                    k_bits=k_bits, bias=bias, bands=list(cfg["bands"]))
+                    k_bits=k_bits, bias=bias, bands=list(cfg["bands"]), seed=int(cfg["seed"]))
+
+
+def make_values(w: "Workload") -> np.ndarray:
+    """Value rows for a workload, bf16 bits [B, Hkv, T, D]: N(0, 1) per element from the
+    stream ``default_rng([seed, b, h, 1])`` (independent of the Q/K streams)."""
+    v = np.empty((w.B, w.Hkv, w.T, w.D), dtype=np.uint16)
+    for b in range(w.B):
+        for h in range(w.Hkv):
+            rng = np.random.default_rng([w.seed, b, h, 1])
+            v[b, h] = bf16_round_bits(rng.standard_normal((w.T, w.D), dtype=np.float32))
+    return v
+
+
+def make_scores(w: "Workload") -> np.ndarray:
+    """Per-token scorer outputs r[b, h, t] (float32 [B, Hkv, T]) standing in for a
+    learned scorer's predictions: N(0, 1) from ``default_rng([seed, b, h, 2])``."""
+    r = np.empty((w.B, w.Hkv, w.T), dtype=np.float32)
+    for b in range(w.B):
+        for h in range(w.Hkv):
+            r[b, h] = np.random.default_rng([w.seed, b, h, 2]).standard_normal(w.T, dtype=np.float32)
+    return r
