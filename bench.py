@@ -286,6 +286,43 @@ def main():
     topk = {"budget": {"sinks": s_, "window": w_, "k": k_}, "steps": n_tk, "ms": round(tk_ms, 4),
             "tokens_per_s": w.B * w.Hkv * w.T / (tk_ms * 1e-3)}
 
+    # Running top-k sparse attention forward (Sec. 3.2, App. C) under that budget's
+    # mask, then pass 2 from its sparse LSE (App. D.3): the paper's training-time
+    # target, which needs no dense pass 1.
+    tk = kv.kvpop_running_topk(scores, s_, w_, k_, log_gamma=lg, labels=False, evict=True, workspace=ws)
+    evict = tk["evict"]
+    v = torch.from_numpy(workload.make_values(w).view(np.int16)).view(torch.bfloat16).to(dev)
+    o_sp = torch.empty_like(q)
+    lse_sp = torch.empty(shape, dtype=torch.float32, device=dev)
+    mass_sp = torch.empty(shape, dtype=torch.float32, device=dev)
+    tt = torch.arange(w.T, device=dev, dtype=torch.int64)
+    kept_pairs = int((evict.to(torch.int64).clamp(max=w.T) - tt).clamp(min=0).sum()) * w.G
+    for _ in range(2):
+        kv.kvpop_sparse_attn_fwd(q, k, v, evict, w.scale, key_bias=bias, o=o_sp, lse=lse_sp)
+    n_sp = max(1, args.steps // 2)
+    ev_sp = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n_sp)]
+    win0, hor0 = w.bands[0]
+    for i in range(n_sp):
+        ev_sp[i][0].record()
+        kv.kvpop_sparse_attn_fwd(q, k, v, evict, w.scale, key_bias=bias, o=o_sp, lse=lse_sp)
+        ev_sp[i][1].record()
+        kv.kvpop_future_attn_from_lse(q, k, lse_sp, w.scale, win0, hor0, key_bias=bias, out=mass_sp)
+        ev_sp[i][2].record()
+    torch.cuda.synchronize()
+    sp_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev_sp]))
+    p2s_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev_sp]))
+    assert bool(torch.isfinite(lse_sp).all()), "sparse LSE not finite"
+    sp_flops = 4.0 * w.D * kept_pairs
+    sp_tf = sp_flops / (sp_ms * 1e-3) / 1e12
+    sparse = {"budget": {"sinks": s_, "window": w_, "k": k_}, "steps": n_sp, "ms": round(sp_ms, 4),
+              "kept_pairs": kept_pairs, "pairs_per_s": kept_pairs / (sp_ms * 1e-3),
+              "roofline": {"bound": "mfma", "achieved": round(sp_tf, 2), "peak": PEAK_BF16_TFLOPS,
+                           "unit": "TFLOP/s", "frac": round(sp_tf / PEAK_BF16_TFLOPS, 4),
+                           "traffic": traffic_for("sparse_attn_fwd_kernel", w.name),
+                           "kernel": "sparse_attn_fwd_kernel", "avg_launch_ms": round(sp_ms, 4)},
+              "pass2_from_sparse_lse_ms": round(p2s_ms, 4)}
+    del v, o_sp, mass_sp
+
     # Parity sanity on the live result: full-future masses of a head sum to T.
     for i, (a, b) in enumerate(w.bands):
         if a == 0 and b < 0:
@@ -320,6 +357,7 @@ def main():
         "roofline": roofline,
         "target_epilogue": epi,
         "running_topk": topk,
+        "sparse_attention": sparse,
         "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)
