@@ -58,7 +58,8 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kRsrcWord3 = 0x00020000;  // raw (untyped) buffer access
-constexpr float kRescale = 8.0f;        // lazy-maximum slack, log2 units
+constexpr float kRescale = 8.0f;        // lazy-maximum slack of the exact variant, log2 units
+constexpr float kOverflow = 64.0f;      // fast variant: largest term above the reference, log2 units
 constexpr int kThreads = 256;
 constexpr int kScan = 4 * kThreads;     // positions per scan step
 constexpr int kCapA = 4096;             // list A capacity (entries)
@@ -115,7 +116,7 @@ struct Smem {
   alignas(16) int scan_sh[4];
 };
 
-template <int D, int HPW, bool HAS_BIAS>
+template <int D, int HPW, bool HAS_BIAS, bool EXACT>
 __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(1, 1))) void
 sparse_attn_fwd_kernel(SparseLaunch a) {
   using SM = Smem<D, HAS_BIAS>;
@@ -150,6 +151,15 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
     qrow[c] = q0 + 32 * qblk + col;
   }
 
+  // The exact variant only redoes tiles the fast variant flagged (NaN in lse).
+  if (EXACT) {
+    int flagged = 0;
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+      if (qrow[c] < T) flagged |= __builtin_isnan(a.lse[((size_t)b * a.Hq + qh[c]) * T + qrow[c]]);
+    if (!__syncthreads_or(flagged)) return;
+  }
+
   // Q columns in registers as the B operand of S^T = K Q^T: k-step s uses the
   // 16-byte chunk 2 s + hi of the query row.
   bf16x8 qf[2][KS];
@@ -167,6 +177,7 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
     for (int d = 0; d < DB; ++d) o[c][d] = f32x16{};
   float m[2] = {-__builtin_inff(), -__builtin_inff()};
   float l[2] = {0.f, 0.f};
+  bool ovf[2] = {false, false};
 
   const size_t kvoff = (size_t)bh * T * D;
   const int kv_bytes = T * D * 2;
@@ -222,13 +233,17 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
       sacc[0] = mfma32(af, qf[0][s], sacc[0]);
       sacc[1] = mfma32(af, qf[1][s], sacc[1]);
     }
-    // Logits in log2 units, in place.
+    // With a key bias, logits in log2 units in place; without one the raw scores
+    // stay (the scale is positive, so their maximum is the logits' maximum) and the
+    // scale is folded into the exponential's fma.
     f32x16 (&x)[2] = sacc;
+    if (HAS_BIAS) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const float b2 = HAS_BIAS ? sm.btile[buf][acc_row(r, hi)] * kLog2e : 0.f;
+      for (int r = 0; r < 16; ++r) {
+        const float b2 = sm.btile[buf][acc_row(r, hi)] * kLog2e;
 #pragma unroll
-      for (int c = 0; c < 2; ++c) x[c][r] = HAS_BIAS ? sacc[c][r] * a.c + b2 : sacc[c][r] * a.c;
+        for (int c = 0; c < 2; ++c) x[c][r] = __builtin_fmaf(sacc[c][r], a.c, b2);
+      }
     }
     if (masked || e0 + 32 > n) {
 #pragma unroll
@@ -259,18 +274,27 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
       float m0, m1;
       pair_values(mx, m0, m1);
       mx = fmaxf(m0, m1);
-      if (mx > m[c] + kRescale) {
-        const float f = __builtin_amdgcn_exp2f(m[c] - mx);
+      if (!HAS_BIAS) mx *= a.c;  // log2 units
+      if (EXACT) {
+        // Online maximum with lazy rescaling of the accumulators.
+        if (mx > m[c] + kRescale) {
+          const float f = __builtin_amdgcn_exp2f(m[c] - mx);
 #pragma unroll
-        for (int d = 0; d < DB; ++d) o[c][d] *= f;
-        l[c] *= f;
-        m[c] = mx;
+          for (int d = 0; d < DB; ++d) o[c][d] *= f;
+          l[c] *= f;
+          m[c] = mx;
+        }
+      } else {
+        // Fixed reference: the first finite block maximum. Later terms up to 2^64
+        // are exact in fp32 and bf16; beyond that the tile is flagged.
+        if (m[c] == -__builtin_inff()) m[c] = mx;
+        ovf[c] = ovf[c] || mx > m[c] + kOverflow;
       }
       const float mu = m[c] == -__builtin_inff() ? 0.f : m[c];
       float p[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        p[r] = __builtin_amdgcn_exp2f(x[c][r] - mu);
+        p[r] = HAS_BIAS ? __builtin_amdgcn_exp2f(x[c][r] - mu) : __builtin_amdgcn_exp2f(__builtin_fmaf(x[c][r], a.c, -mu));
         l[c] += p[r];
       }
 #pragma unroll
@@ -385,15 +409,19 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
   }
 
   // Epilogue: combine the two lane halves' sums, normalise, write O (bf16) and LSE.
+  // A fast-variant column whose terms overflowed the fixed reference writes NaN to
+  // its LSE instead; the exact variant then recomputes the whole tile.
 #pragma unroll
   for (int c = 0; c < 2; ++c) {
     float l0, l1;
     pair_values(l[c], l0, l1);
     const float lt = l0 + l1;
     const float inv = lt > 0.f ? 1.0f / lt : 0.f;
+    const bool redo = !EXACT && __builtin_amdgcn_ballot_w64(ovf[c]) != 0;
     if (qrow[c] >= T) continue;
     const size_t rowi = ((size_t)b * a.Hq + qh[c]) * T + qrow[c];
-    if (hi == 0) a.lse[rowi] = lt > 0.f ? (m[c] + __builtin_amdgcn_logf(lt)) * kLn2 : -__builtin_inff();
+    if (hi == 0)
+      a.lse[rowi] = redo ? __builtin_nanf("") : lt > 0.f ? (m[c] + __builtin_amdgcn_logf(lt)) * kLn2 : -__builtin_inff();
     uint16_t* orow = a.o + rowi * D;
 #pragma unroll
     for (int d = 0; d < DB; ++d) {
@@ -410,10 +438,17 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
   }
 }
 
+// The fast variant, then the exact one, which exits at once on tiles the fast one
+// did not flag.
 template <int D, int HPW, bool HB>
 int launch_d(const SparseLaunch& L) {
   const unsigned grid = (unsigned)((long long)L.ntiles * L.B * L.Hkv * L.nch);
-  hipLaunchKernelGGL((sparse_attn_fwd_kernel<D, HPW, HB>), dim3(grid), dim3(kThreads), 0, (hipStream_t)L.stream, L);
+  hipLaunchKernelGGL((sparse_attn_fwd_kernel<D, HPW, HB, false>), dim3(grid), dim3(kThreads), 0,
+                     (hipStream_t)L.stream, L);
+  int e = (int)hipGetLastError();
+  if (e) return e;
+  hipLaunchKernelGGL((sparse_attn_fwd_kernel<D, HPW, HB, true>), dim3(grid), dim3(kThreads), 0,
+                     (hipStream_t)L.stream, L);
   return (int)hipGetLastError();
 }
 

@@ -204,3 +204,29 @@ def test_paper_budget_at_benchmark_size():
             _check_rows(full, lse_full, wl.q_bits[b, qh], wl.k_bits[b, h], v_bits[b, h], wl.scale, M, rows,
                         wl.bias, "b%d qh%d" % (b, qh))
     assert torch.isfinite(lse).all()
+
+
+def test_large_logits_take_the_exact_path():
+    """Keys after position 100 scaled by 16 (exact in bf16): their logits exceed the
+    first block's maximum by far more than 2^64, so the fast variant flags its tiles
+    and the exact variant (online rescaling) recomputes them. Dense causal lifetimes."""
+    T, D = 300, 128
+    wl = workload.make(_cfg(1, 4, 1, T, D, seed=13))
+    k_bits = wl.k_bits.copy()
+    kf = k_bits.view(np.uint16).astype(np.uint32) << 16
+    kf = kf.view(np.float32)
+    kf[:, :, 100:] *= 16.0
+    k_bits = (kf.view(np.uint32) >> 16).astype(np.uint16)
+    v_bits = workload.make_values(wl)
+    ev = torch.full((1, 1, T), T, dtype=torch.int32, device="cuda")
+    o, lse = kv.kvpop_sparse_attn_fwd(_dev(wl.q_bits), _dev(k_bits), _dev(v_bits), ev, wl.scale)
+    torch.cuda.synchronize()
+    o = _bf16_to_f64(o)
+    lse = lse.cpu().numpy().astype(np.float64)
+    rows = np.arange(T)
+    M = oracle.lifetime_mask(np.full(T, T), rows)
+    _, lse_ref, _ = oracle.sparse_attention(wl.q_bits[0, 0], k_bits[0, 0], v_bits[0, 0], wl.scale, M)
+    assert (lse_ref[150:] - lse_ref[:32].max()).max() * 1.4427 > 64  # the case is what it claims to be
+    for qh in range(4):
+        _check_rows(o[0, qh], lse[0, qh], wl.q_bits[0, qh], k_bits[0, 0], v_bits[0, 0],
+                    wl.scale, M, rows, None, "qh%d" % qh)
