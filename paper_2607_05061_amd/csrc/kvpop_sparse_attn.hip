@@ -26,17 +26,18 @@
 //   O^T += V^T P^T  the probabilities leave the S accumulators already in the B
 //                   operand layout (the key order inside a k-step is free), and
 //                   V^T comes from ds_read_b64_tr_b16 over row-major V planes.
-// The running maximum is lazy: it is raised (and O, l rescaled) only when a block's
-// maximum exceeds it by more than 2^8, so the common block costs one fma, one exp
-// and one add per element plus the bf16 packing.
+// Each query keeps a fixed reference maximum (its first finite block's), so the
+// accumulators are only ever touched by MFMAs; a column whose later logits exceed
+// it by more than 2^64 is flagged and recomputed by an exact variant with the
+// usual online rescaling.
 //
-// Workgroup = (batch b, KV head h, head chunk, query tile); 4 waves, each holding
-// two (head, 32-query) columns: two heads of the same queries when G >= 2, so both
-// MFMA chains of a wave share every K and V fragment read from LDS, and the same
-// 32-key block serves all heads of the chunk (the GQA sharing). K and V rows are
-// gathered by their positions straight from global memory into LDS
-// (buffer_load ... lds, one 1 KB plane per instruction); a buffer descriptor's range
-// check turns padding rows into zeros.
+// Workgroup = (batch b, KV head h, head chunk, query tile): 8 waves, two per SIMD,
+// each owning one (head, 32-query) column; for G >= 2 the columns are the heads
+// of a head chunk times the tile's 32-query blocks, so every 32-key block in LDS
+// serves all of them (the GQA sharing). Two waves per SIMD hide each other's MFMA,
+// LDS and barrier latency. K and V rows are gathered by their positions straight
+// from global memory into LDS (buffer_load ... lds, one 1 KB plane per
+// instruction); a buffer descriptor's range check turns padding rows into zeros.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -51,25 +52,52 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
-typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kRsrcWord3 = 0x00020000;  // raw (untyped) buffer access
 constexpr float kRescale = 8.0f;        // lazy-maximum slack of the exact variant, log2 units
 constexpr float kOverflow = 64.0f;      // fast variant: largest term above the reference, log2 units
-constexpr int kThreads = 256;
-constexpr int kScan = 4 * kThreads;     // positions per scan step
+constexpr int kWaves = 8;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kScan = 1024;             // positions per scan step (2 per thread)
 constexpr int kCapA = 4096;             // list A capacity (entries)
 constexpr int kCapP = 1536;             // list P capacity (entries)
 constexpr int kPlane = 512;             // bf16 elements per 1 KB plane
+constexpr int kBufs = 4;                // K/V block buffers (see the block loop)
+constexpr int kChunk = 4096;            // lifetimes staged into LDS per chunk (16 KB)
+constexpr int kEvBufs = 2;              // chunk buffers: the next chunk loads during the scan
 
 __device__ __forceinline__ constexpr int acc_row(int r, int hi) { return 8 * (r >> 2) + 4 * hi + (r & 3); }
 
 __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+
+// Workgroup barrier for the loops. __syncthreads() (and even an LDS-only fence)
+// makes the compiler wait for every outstanding buffer load, because loads into
+// LDS count as LDS writes; that would also wait for the prefetch of later blocks.
+// Every wave waits for its own copies with vmcnt before arriving and has consumed
+// its LDS reads of any buffer about to be refilled, so a bare s_barrier suffices;
+// the memory clobber keeps the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// Barrier after this wave's LDS writes have completed (lgkmcnt(0)), without
+// waiting for outstanding buffer loads.
+__device__ __forceinline__ void lds_sync() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt at their maxima
+  block_barrier();
 }
 
 // (x of lane l % 32, x of lane l % 32 + 32) on every lane.
@@ -80,26 +108,59 @@ __device__ __forceinline__ void pair_values(float x, float& a, float& b) {
   b = __int_as_float(r[1]);
 }
 
-// Exclusive prefix sum over the 256 threads; `total` gets the sum. `sh` holds 4 ints.
-__device__ __forceinline__ int block_excl_scan(int v, int* sh, int& total) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  int x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
-  if (lane == 63) sh[w] = x;
-  __syncthreads();
-  int pre = 0, tot = 0;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int t = sh[i];
-    pre += i < w ? t : 0;
-    tot += t;
-  }
-  total = tot;
-  return pre + x - v;
+// The transposing V reads of a block (the A operands of O^T += V^T P^T; plane
+// layout at the kernel's pv). They are issued from inline asm so that the
+// compiler, which cannot tell which LDS buffer a transposing read touches, does not
+// wait for every outstanding buffer load (including the prefetches of later blocks)
+// before them. Their registers are valid only after vfrag_wait, whose
+// read-modify-write operands keep every use behind the wait.
+template <int DB>
+struct VFrag {
+  i16x4 r[DB * 4];  // [d][k2][half]
+};
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
+}
+
+__device__ __forceinline__ void vfrag_issue(VFrag<4>& f, uint32_t a) {
+  asm volatile(
+      "ds_read_b64_tr_b16 %0, %16 offset:0\n ds_read_b64_tr_b16 %1, %16 offset:512\n"
+      "ds_read_b64_tr_b16 %2, %16 offset:4096\n ds_read_b64_tr_b16 %3, %16 offset:4608\n"
+      "ds_read_b64_tr_b16 %4, %16 offset:1024\n ds_read_b64_tr_b16 %5, %16 offset:1536\n"
+      "ds_read_b64_tr_b16 %6, %16 offset:5120\n ds_read_b64_tr_b16 %7, %16 offset:5632\n"
+      "ds_read_b64_tr_b16 %8, %16 offset:2048\n ds_read_b64_tr_b16 %9, %16 offset:2560\n"
+      "ds_read_b64_tr_b16 %10, %16 offset:6144\n ds_read_b64_tr_b16 %11, %16 offset:6656\n"
+      "ds_read_b64_tr_b16 %12, %16 offset:3072\n ds_read_b64_tr_b16 %13, %16 offset:3584\n"
+      "ds_read_b64_tr_b16 %14, %16 offset:7168\n ds_read_b64_tr_b16 %15, %16 offset:7680"
+      : "=&v"(f.r[0]), "=&v"(f.r[1]), "=&v"(f.r[2]), "=&v"(f.r[3]), "=&v"(f.r[4]), "=&v"(f.r[5]), "=&v"(f.r[6]),
+        "=&v"(f.r[7]), "=&v"(f.r[8]), "=&v"(f.r[9]), "=&v"(f.r[10]), "=&v"(f.r[11]), "=&v"(f.r[12]),
+        "=&v"(f.r[13]), "=&v"(f.r[14]), "=&v"(f.r[15])
+      : "v"(a));
+}
+
+__device__ __forceinline__ void vfrag_wait(VFrag<4>& f) {
+  asm volatile("s_waitcnt lgkmcnt(0)"
+               : "+v"(f.r[0]), "+v"(f.r[1]), "+v"(f.r[2]), "+v"(f.r[3]), "+v"(f.r[4]), "+v"(f.r[5]), "+v"(f.r[6]),
+                 "+v"(f.r[7]), "+v"(f.r[8]), "+v"(f.r[9]), "+v"(f.r[10]), "+v"(f.r[11]), "+v"(f.r[12]),
+                 "+v"(f.r[13]), "+v"(f.r[14]), "+v"(f.r[15]));
+}
+
+__device__ __forceinline__ void vfrag_issue(VFrag<2>& f, uint32_t a) {
+  asm volatile(
+      "ds_read_b64_tr_b16 %0, %8 offset:0\n ds_read_b64_tr_b16 %1, %8 offset:512\n"
+      "ds_read_b64_tr_b16 %2, %8 offset:2048\n ds_read_b64_tr_b16 %3, %8 offset:2560\n"
+      "ds_read_b64_tr_b16 %4, %8 offset:1024\n ds_read_b64_tr_b16 %5, %8 offset:1536\n"
+      "ds_read_b64_tr_b16 %6, %8 offset:3072\n ds_read_b64_tr_b16 %7, %8 offset:3584"
+      : "=&v"(f.r[0]), "=&v"(f.r[1]), "=&v"(f.r[2]), "=&v"(f.r[3]), "=&v"(f.r[4]), "=&v"(f.r[5]), "=&v"(f.r[6]),
+        "=&v"(f.r[7])
+      : "v"(a));
+}
+
+__device__ __forceinline__ void vfrag_wait(VFrag<2>& f) {
+  asm volatile("s_waitcnt lgkmcnt(0)"
+               : "+v"(f.r[0]), "+v"(f.r[1]), "+v"(f.r[2]), "+v"(f.r[3]), "+v"(f.r[4]), "+v"(f.r[5]), "+v"(f.r[6]),
+                 "+v"(f.r[7]));
 }
 
 template <int D, bool HAS_BIAS>
@@ -107,22 +168,22 @@ struct Smem {
   static constexpr int KS = D / 16;  // K planes per block (k-steps over the head dim)
   static constexpr int DB = D / 32;  // 32-row blocks of the head dim
   static constexpr int VP = 2 * DB;  // V planes per block
-  alignas(16) uint16_t ktile[2][KS * kPlane];
-  alignas(16) uint16_t vtile[2][VP * kPlane];
-  alignas(16) float btile[2][HAS_BIAS ? 64 : 4];
+  alignas(16) uint16_t ktile[kBufs][KS * kPlane];
+  alignas(16) uint16_t vtile[kBufs][VP * kPlane];
+  alignas(16) float btile[kBufs][HAS_BIAS ? 64 : 4];
+  alignas(16) int evs[kEvBufs][kChunk];  // lifetimes of the positions being scanned
   alignas(16) int listA[kCapA];
   alignas(16) int posP[kCapP];  // read 16 bytes at a time
   alignas(16) int lenP[kCapP];
-  alignas(16) int scan_sh[4];
+  alignas(16) int scan_sh[2][32];
 };
 
 template <int D, int HPW, bool HAS_BIAS, bool EXACT>
-__global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(1, 1))) void
+__global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(2, 2))) void
 sparse_attn_fwd_kernel(SparseLaunch a) {
   using SM = Smem<D, HAS_BIAS>;
-  constexpr int KS = SM::KS, DB = SM::DB, VP = SM::VP;
-  constexpr int KPW = KS / 4, VPW = VP / 4;  // planes each wave copies per block
-  static_assert(KPW >= 1 && VPW >= 1, "head dim");
+  constexpr int KS = SM::KS, DB = SM::DB;
+  static_assert(KS == 4 || KS == 8, "head dim 64 or 128");
   __shared__ __attribute__((aligned(16))) SM sm;
 
   const int tid = threadIdx.x;
@@ -130,54 +191,53 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
   const int lane = tid & 63, hi = lane >> 5, col = lane & 31;
   const int T = a.T;
 
-  // Heaviest tiles first; consecutive workgroups cover different (b, h, chunk)
-  // groups of the same tile, so blockIdx % 8 (the XCD) follows the group.
+  // Workgroup order. Workgroups are dealt to the 8 XCDs round-robin (XCD =
+  // blockIdx % 8). When the (b, h, chunk) groups divide evenly, each XCD takes its
+  // share of groups one after another, heaviest tile first, so the tiles running
+  // together on an XCD belong to one group and share its keys in that XCD's L2;
+  // otherwise groups interleave within each tile.
   const int groups = a.B * a.Hkv * a.nch;
-  const int tile = a.ntiles - 1 - (int)(blockIdx.x / groups);
-  const int grp = (int)(blockIdx.x % groups);
+  int tile, grp;
+  if ((groups & 7) == 0) {
+    const int x = (int)(blockIdx.x & 7), j = (int)(blockIdx.x >> 3);
+    tile = a.ntiles - 1 - j % a.ntiles;
+    grp = x + 8 * (j / a.ntiles);
+  } else {
+    tile = a.ntiles - 1 - (int)(blockIdx.x / groups);
+    grp = (int)(blockIdx.x % groups);
+  }
   const int bh = grp / a.nch, chunk = grp % a.nch;
   const int b = bh / a.Hkv, h = bh % a.Hkv;
   const int q0 = tile * a.qt;
   const int q1 = min(q0 + a.qt, T) - 1;
 
-  // This wave's two (head, 32-query) columns.
-  const int hg = wave / a.wq, wq = wave % a.wq;
-  int qh[2], qrow[2];
-#pragma unroll
-  for (int c = 0; c < 2; ++c) {
-    const int head = chunk * a.hc + hg * HPW + (HPW == 2 ? c : 0);
-    const int qblk = HPW == 2 ? wq : 2 * wq + c;
-    qh[c] = h * a.G + head;
-    qrow[c] = q0 + 32 * qblk + col;
-  }
+  // This wave's (head, 32-query) column: columns 2 u and 2 u + 1 are two heads of
+  // the same queries when G >= 2, two query blocks of one head otherwise.
+  const int u = wave >> 1, cc = wave & 1;
+  const int hg = u / a.wq, wq = u % a.wq;
+  const int qh = h * a.G + chunk * a.hc + hg * HPW + (HPW == 2 ? cc : 0);
+  const int qrow = q0 + 32 * (HPW == 2 ? wq : 2 * wq + cc) + col;
 
   // The exact variant only redoes tiles the fast variant flagged (NaN in lse).
   if (EXACT) {
-    int flagged = 0;
-#pragma unroll
-    for (int c = 0; c < 2; ++c)
-      if (qrow[c] < T) flagged |= __builtin_isnan(a.lse[((size_t)b * a.Hq + qh[c]) * T + qrow[c]]);
+    const int flagged = qrow < T ? __builtin_isnan(a.lse[((size_t)b * a.Hq + qh) * T + qrow]) : 0;
     if (!__syncthreads_or(flagged)) return;
   }
 
-  // Q columns in registers as the B operand of S^T = K Q^T: k-step s uses the
+  // Q column in registers as the B operand of S^T = K Q^T: k-step s uses the
   // 16-byte chunk 2 s + hi of the query row.
-  bf16x8 qf[2][KS];
+  bf16x8 qf[KS];
+  {
+    const uint16_t* row = a.q + (((size_t)b * a.Hq + qh) * T + min(qrow, T - 1)) * D;
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
-    const uint16_t* row = a.q + (((size_t)b * a.Hq + qh[c]) * T + min(qrow[c], T - 1)) * D;
-#pragma unroll
-    for (int s = 0; s < KS; ++s) qf[c][s] = *reinterpret_cast<const bf16x8*>(row + (2 * s + hi) * 8);
+    for (int s = 0; s < KS; ++s) qf[s] = *reinterpret_cast<const bf16x8*>(row + (2 * s + hi) * 8);
   }
 
-  f32x16 o[2][DB];
+  f32x16 o[DB];
 #pragma unroll
-  for (int c = 0; c < 2; ++c)
-#pragma unroll
-    for (int d = 0; d < DB; ++d) o[c][d] = f32x16{};
-  float m[2] = {-__builtin_inff(), -__builtin_inff()};
-  float l[2] = {0.f, 0.f};
-  bool ovf[2] = {false, false};
+  for (int d = 0; d < DB; ++d) o[d] = f32x16{};
+  float m = -__builtin_inff(), l = 0.f;
+  bool ovf = false;
 
   const size_t kvoff = (size_t)bh * T * D;
   const int kv_bytes = T * D * 2;
@@ -189,30 +249,31 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
       __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.bias), (short)0, HAS_BIAS ? T * 4 : 0, kRsrcWord3);
   const int32_t* ev = a.evict + (size_t)bh * T;
 
-  // V row and column chunk this lane copies into a V plane (see compute_block for
-  // the layout the transposing read expects).
-  const int ks2_w = (wave * VPW) / DB;
-  const int vrow = 16 * ks2_w + 8 * hi + 4 * (col >> 4) + ((lane & 7) >> 1);
+  // The 1 KB planes this wave copies per block: K plane `wave` (if any) and one V
+  // plane (D = 128: K plane w and V plane w; D = 64: K plane w for w < 4, V plane
+  // w - 4 for the others), plus the block's key biases for wave 0.
+  const int kplane = wave < KS ? wave : -1;
+  const int vplane = KS == 8 ? wave : (wave >= KS ? wave - KS : -1);
+  const int nload = (kplane >= 0) + (vplane >= 0) + (HAS_BIAS && wave == 0);
+  // V row and column chunk this lane copies into its V plane (layout at pv).
+  const int vrow = 16 * (max(vplane, 0) / DB) + 8 * hi + 4 * (col >> 4) + ((lane & 7) >> 1);
   const int vcol_bytes = (16 * ((lane >> 3) & 1) + 8 * (lane & 1)) * 2;
 
-  // Gather the 32 keys of block `blk` of `lpos` (n entries) into buffer `buf`.
-  auto issue = [&](const int* lpos, int n, int blk, int buf) __attribute__((always_inline)) {
+  // Gather the 32 keys of block `blk` of `lpos` into buffer `buf`. The lists are
+  // padded to whole blocks with position -1, which reads as zero rows.
+  auto issue = [&](const int* lpos, int blk, int buf) __attribute__((always_inline)) {
     const int e0 = blk * 32;
-    const int pk = e0 + col < n ? lpos[e0 + col] : -1;
-    const int pv = e0 + vrow < n ? lpos[e0 + vrow] : -1;
-    const int voffK = pk >= 0 ? pk * (D * 2) + hi * 16 : kv_bytes;
-    const int voffV = pv >= 0 ? pv * (D * 2) + vcol_bytes : kv_bytes;
-#pragma unroll
-    for (int i = 0; i < KPW; ++i) {
-      const int s = wave * KPW + i;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_ptr_t)(sm.ktile[buf] + s * kPlane), 16, voffK, s * 32, 0,
-                                               0);
+    const int pk = lpos[e0 + col];
+    if (kplane >= 0) {
+      const int voffK = pk >= 0 ? pk * (D * 2) + hi * 16 : kv_bytes;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_ptr_t)(sm.ktile[buf] + kplane * kPlane), 16, voffK,
+                                               kplane * 32, 0, 0);
     }
-#pragma unroll
-    for (int i = 0; i < VPW; ++i) {
-      const int idx = wave * VPW + i;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_ptr_t)(sm.vtile[buf] + idx * kPlane), 16, voffV,
-                                               (idx % DB) * 64, 0, 0);
+    if (vplane >= 0) {
+      const int pv = lpos[e0 + vrow];
+      const int voffV = pv >= 0 ? pv * (D * 2) + vcol_bytes : kv_bytes;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_ptr_t)(sm.vtile[buf] + vplane * kPlane), 16, voffV,
+                                               (vplane % DB) * 64, 0, 0);
     }
     if (HAS_BIAS && wave == 0) {
       const int voffB = pk >= 0 ? pk * 4 : T * 4;
@@ -220,112 +281,137 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
     }
   };
 
-  // One 32-key block from buffer `buf`. MASKED: per-element lifetimes from
-  // (lpos, llen); otherwise only padding rows (entries >= n) are masked.
-  auto compute_block = [&](const int* lpos, const int* llen, bool masked, int n, int blk,
-                           int buf) __attribute__((always_inline)) {
-    const int e0 = blk * 32;
-    f32x16 sacc[2] = {f32x16{}, f32x16{}};
+  // Wait until the oldest outstanding block's copies have landed, given how many
+  // later blocks this wave has issued (buffer loads complete in order).
+  auto wait_block = [&](int later) __attribute__((always_inline)) {
+    switch (later * nload) {
+      case 0: wait_vmcnt<0>(); break;
+      case 1: wait_vmcnt<1>(); break;
+      case 2: wait_vmcnt<2>(); break;
+      case 3: wait_vmcnt<3>(); break;
+      case 4: wait_vmcnt<4>(); break;
+      case 5: wait_vmcnt<5>(); break;
+      default: wait_vmcnt<6>(); break;
+    }
+  };
+
+  // S^T = K Q^T of the block in buffer `buf`.
+  auto qk = [&](int buf, f32x16& sacc) __attribute__((always_inline)) {
+    sacc = f32x16{};
     const uint16_t* kt = sm.ktile[buf];
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      const bf16x8 af = *reinterpret_cast<const bf16x8*>(kt + s * kPlane + lane * 8);
-      sacc[0] = mfma32(af, qf[0][s], sacc[0]);
-      sacc[1] = mfma32(af, qf[1][s], sacc[1]);
-    }
-    // With a key bias, logits in log2 units in place; without one the raw scores
-    // stay (the scale is positive, so their maximum is the logits' maximum) and the
-    // scale is folded into the exponential's fma.
-    f32x16 (&x)[2] = sacc;
+    for (int s = 0; s < KS; ++s)
+      sacc = mfma32(*reinterpret_cast<const bf16x8*>(kt + s * kPlane + lane * 8), qf[s], sacc);
+  };
+
+  // Key bias and masking of block `blk` of a list (entries lpos/llen, n of them):
+  // with a bias, logits in log2 units in place; without one the raw scores stay
+  // (the scale is positive, so their maximum is the logits' maximum) and the scale
+  // is folded into the exponential's fma.
+  auto prep = [&](f32x16& x, const int* lpos, const int* llen, bool masked, int n, int blk, int buf)
+                  __attribute__((always_inline)) {
+    const int e0 = blk * 32;
     if (HAS_BIAS) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float b2 = sm.btile[buf][acc_row(r, hi)] * kLog2e;
-#pragma unroll
-        for (int c = 0; c < 2; ++c) x[c][r] = __builtin_fmaf(sacc[c][r], a.c, b2);
-      }
+      for (int r = 0; r < 16; ++r) x[r] = __builtin_fmaf(x[r], a.c, sm.btile[buf][acc_row(r, hi)] * kLog2e);
     }
-    if (masked || e0 + 32 > n) {
+    if (masked) {
+      // List P: kept iff t <= q < t + len, i.e. (unsigned)(q - t) < len; padding
+      // entries have len 0.
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int e = e0 + 8 * g + 4 * hi;
-        i32x4 pp = {0, 0, 0, 0}, ll = {0, 0, 0, 0};
-        if (masked) {
-          pp = *reinterpret_cast<const i32x4*>(lpos + e);
-          ll = *reinterpret_cast<const i32x4*>(llen + e);
-        }
+        const i32x4 pp = *reinterpret_cast<const i32x4*>(lpos + e);
+        const i32x4 ll = *reinterpret_cast<const i32x4*>(llen + e);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const bool valid = e + j < n;
-#pragma unroll
-          for (int c = 0; c < 2; ++c) {
-            const bool keep = valid && (!masked || (unsigned)(qrow[c] - pp[j]) < (unsigned)ll[j]);
-            x[c][4 * g + j] = keep ? x[c][4 * g + j] : -__builtin_inff();
-          }
-        }
+        for (int j = 0; j < 4; ++j)
+          x[4 * g + j] = (unsigned)(qrow - pp[j]) < (unsigned)ll[j] ? x[4 * g + j] : -__builtin_inff();
       }
+    } else if (e0 + 32 > n) {
+      // The last block of list A: padding rows only.
+#pragma unroll
+      for (int r = 0; r < 16; ++r) x[r] = e0 + acc_row(r, hi) < n ? x[r] : -__builtin_inff();
     }
-    bf16x8 pk[2][2];
+  };
+
+  // Softmax numerators of a block: reference maximum, exponentials, row sum and
+  // bf16 packing into the B operand of the PV product.
+  auto softmax = [&](f32x16& x, bf16x8 (&pk)[2]) __attribute__((always_inline)) {
+    float mx = x[0];
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      float mx = x[c][0];
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, x[r]);
+    float m0, m1;
+    pair_values(mx, m0, m1);
+    mx = fmaxf(m0, m1);
+    if (!HAS_BIAS) mx *= a.c;  // log2 units
+    if (EXACT) {
+      // Online maximum with lazy rescaling of the accumulators.
+      if (mx > m + kRescale) {
+        const float f = __builtin_amdgcn_exp2f(m - mx);
 #pragma unroll
-      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, x[c][r]);
-      float m0, m1;
-      pair_values(mx, m0, m1);
-      mx = fmaxf(m0, m1);
-      if (!HAS_BIAS) mx *= a.c;  // log2 units
-      if (EXACT) {
-        // Online maximum with lazy rescaling of the accumulators.
-        if (mx > m[c] + kRescale) {
-          const float f = __builtin_amdgcn_exp2f(m[c] - mx);
-#pragma unroll
-          for (int d = 0; d < DB; ++d) o[c][d] *= f;
-          l[c] *= f;
-          m[c] = mx;
-        }
-      } else {
-        // Fixed reference: the first finite block maximum. Later terms up to 2^64
-        // are exact in fp32 and bf16; beyond that the tile is flagged.
-        if (m[c] == -__builtin_inff()) m[c] = mx;
-        ovf[c] = ovf[c] || mx > m[c] + kOverflow;
+        for (int d = 0; d < DB; ++d) o[d] *= f;
+        l *= f;
+        m = mx;
       }
-      const float mu = m[c] == -__builtin_inff() ? 0.f : m[c];
-      float p[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        p[r] = HAS_BIAS ? __builtin_amdgcn_exp2f(x[c][r] - mu) : __builtin_amdgcn_exp2f(__builtin_fmaf(x[c][r], a.c, -mu));
-        l[c] += p[r];
-      }
-#pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2) {
-        f32x8 v8;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) v8[j] = p[8 * k2 + j];
-        pk[c][k2] = __builtin_convertvector(v8, bf16x8);
-      }
+    } else {
+      // Fixed reference: the first finite block maximum. Later terms up to 2^64 are
+      // exact in fp32 and bf16; beyond that the column is flagged.
+      if (m == -__builtin_inff()) m = mx;
+      ovf = ovf || mx > m + kOverflow;
     }
-    // O^T += V^T P^T. Plane (k2, d) holds, at byte 512 hh + 8 l for lane
-    // l = 16 g + 4 j + i4, the 4 values V[16 k2 + 8 hh + 4 (g / 2) + j][32 d + 16 (g % 2) + 4 i4 ..];
-    // the transposing read then hands lane l the values of head-dim row 32 d + l % 32
-    // for keys 16 k2 + 8 hh + 4 (l / 32) + 0..3, which is its A operand for the
-    // contraction index 8 (l / 32) + 4 hh + j -- the same key order the S^T
-    // accumulators give the B operand.
-    const uint16_t* vt = sm.vtile[buf];
+    const float mu = m == -__builtin_inff() ? 0.f : m;
+    float p[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      p[r] = HAS_BIAS ? __builtin_amdgcn_exp2f(x[r] - mu) : __builtin_amdgcn_exp2f(__builtin_fmaf(x[r], a.c, -mu));
+      l += p[r];
+    }
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) {
+      f32x8 v8;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v8[j] = p[8 * k2 + j];
+      pk[k2] = __builtin_convertvector(v8, bf16x8);
+    }
+  };
+
+  // O^T += V^T P^T. V plane (k2, d) (1 KB at byte 1024 (k2 DB + d) of the block's
+  // V tile) holds, at byte 512 hh + 8 l for lane l = 16 g + 4 j + i4, the 4 values
+  // V[16 k2 + 8 hh + 4 (g / 2) + j][32 d + 16 (g % 2) + 4 i4 ..]; the transposing read
+  // then hands lane l the values of head-dim row 32 d + l % 32 for keys
+  // 16 k2 + 8 hh + 4 (l / 32) + 0..3, which is its A operand for the contraction
+  // index 8 (l / 32) + 4 hh + j -- the same key order the S^T accumulators give the
+  // B operand. Fragment (d, k2) is registers 4 d + 2 k2 (lower half) and + 1.
+  auto pv = [&](const VFrag<DB>& f, const bf16x8 (&pk)[2]) __attribute__((always_inline)) {
 #pragma unroll
     for (int d = 0; d < DB; ++d) {
 #pragma unroll
       for (int k2 = 0; k2 < 2; ++k2) {
-        const uint16_t* pl = vt + (k2 * DB + d) * kPlane;
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(pl + lane * 4));
-        const i16x4 up = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(pl + 256 + lane * 4));
+        const i16x4 lo = f.r[4 * d + 2 * k2], up = f.r[4 * d + 2 * k2 + 1];
         const i16x8 w8 = {lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
-        const bf16x8 af = __builtin_bit_cast(bf16x8, w8);
-        o[0][d] = mfma32(af, pk[0][k2], o[0][d]);
-        o[1][d] = mfma32(af, pk[1][k2], o[1][d]);
+        o[d] = mfma32(__builtin_bit_cast(bf16x8, w8), pk[k2], o[d]);
       }
     }
   };
+
+  // Lifetimes reach LDS in chunks of kChunk positions, one chunk ahead of the scan,
+  // straight from global memory (16 KB per chunk: 2 KB per wave, 2 loads).
+  // Positions past q1 read as 0 (never alive) through the descriptor's range.
+  const __amdgpu_buffer_rsrc_t re =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(ev), (short)0, (q1 + 1) * 4, kRsrcWord3);
+  auto stage = [&](int ch) __attribute__((always_inline)) {
+    int* dst = sm.evs[ch & (kEvBufs - 1)];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int idx = 2 * wave + i;  // 1 KB pieces of 256 positions
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(re, (lds_ptr_t)(dst + idx * 256), 16, lane * 16,
+                                               (ch * kChunk + idx * 256) * 4, 0, 0);
+    }
+  };
+  const int last_chunk = q1 / kChunk;
+  int staged = 0;  // last chunk whose copies were issued
+  stage(0);
+  int sstep = 0;  // scan steps so far (selects the LDS count buffer)
 
   // Windows of key positions [w0, w1): the compaction scan over their lifetimes
   // stops before either list could overflow, and the window's lists are then
@@ -336,73 +422,148 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
     int cntA = 0, cntP = 0;
     int base = w0;
     while (base <= q1 && cntA <= kCapA - kScan && cntP <= kCapP - kScan) {
-      const int p0 = base + 4 * tid;
-      int kind[4], len[4];
-      int nf = 0, np = 0;
+      if ((base & (kChunk - 1)) == 0) {
+        // This chunk has landed once only the next chunk's copies (2 per wave,
+        // issued after it; loads complete in order) are outstanding.
+        const int c = base / kChunk;
+        if (staged > c) wait_vmcnt<2>();
+        else wait_vmcnt<0>();
+        block_barrier();  // for every wave; chunk c - 1's buffer is free
+        if (c + 1 <= last_chunk) stage(staged = c + 1);
+      }
+      // Thread tid looks at positions base + 512 j + tid, so each wave's ballot is
+      // already in position order; wave counts are exchanged once through LDS.
+      const int* evc = sm.evs[(base / kChunk) & (kEvBufs - 1)] + (base & (kChunk - 1));
+      uint64_t bf[2], bp[2];
+      int len[2];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int p = p0 + j;
-        const int e = p <= q1 ? ev[p] : 0;
+      for (int j = 0; j < 2; ++j) {
+        const int p = base + 512 * j + tid;
+        const int e = p <= q1 ? evc[512 * j + tid] : 0;
         const bool alive = p <= q1 && e > max(p, q0);  // kept by some query of the tile
         const bool full = alive && p <= q0 && e > q1;   // kept by all of them
-        kind[j] = full ? 1 : (alive ? 2 : 0);
+        bf[j] = __builtin_amdgcn_ballot_w64(full);
+        bp[j] = __builtin_amdgcn_ballot_w64(alive && !full);
         len[j] = e - p;
-        nf += full;
-        np += alive && !full;
       }
-      int total;
-      const int ex = block_excl_scan(nf | (np << 16), sm.scan_sh, total);
-      int ia = cntA + (ex & 0xFFFF), ip = cntP + (ex >> 16);
+      int* sh = sm.scan_sh[sstep & 1];  // [kind][j][wave]
+      if (lane == 0) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        if (kind[j] == 1) {
-          sm.listA[ia++] = p0 + j;
-        } else if (kind[j] == 2) {
-          sm.posP[ip] = p0 + j;
-          sm.lenP[ip++] = len[j];
+        for (int j = 0; j < 2; ++j) {
+          sh[j * 8 + wave] = __builtin_popcountll(bf[j]);
+          sh[16 + j * 8 + wave] = __builtin_popcountll(bp[j]);
         }
       }
-      __syncthreads();
-      cntA += total & 0xFFFF;
-      cntP += total >> 16;
+      lds_sync();
+      int ia = cntA, ip = cntP;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        int befA = 0, befP = 0, totA = 0, totP = 0;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) {
+          const int ca = sh[j * 8 + w], cp = sh[16 + j * 8 + w];
+          befA += w < wave ? ca : 0;
+          befP += w < wave ? cp : 0;
+          totA += ca;
+          totP += cp;
+        }
+        const int p = base + 512 * j + tid;
+        const int ra = __builtin_amdgcn_mbcnt_hi((uint32_t)(bf[j] >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bf[j], 0));
+        const int rp = __builtin_amdgcn_mbcnt_hi((uint32_t)(bp[j] >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bp[j], 0));
+        if ((bf[j] >> lane) & 1) sm.listA[ia + befA + ra] = p;
+        if ((bp[j] >> lane) & 1) {
+          sm.posP[ip + befP + rp] = p;
+          sm.lenP[ip + befP + rp] = len[j];
+        }
+        ia += totA;
+        ip += totP;
+      }
+      cntA = ia;
+      cntP = ip;
+      ++sstep;
       base += kScan;
     }
+    // Pad both lists to whole blocks: position -1 (zero rows), lifetime 0.
+    if (tid < 32) {
+      if (cntA + tid < ((cntA + 31) & ~31)) sm.listA[cntA + tid] = -1;
+      if (cntP + tid < ((cntP + 31) & ~31)) {
+        sm.posP[cntP + tid] = -1;
+        sm.lenP[cntP + tid] = 0;
+      }
+    }
+    lds_sync();  // the lists are complete and visible to every wave
     w0 = base;
 
-    // Blocks of list A (no per-element test) then of list P, double-buffered:
-    // block i + 1 is gathered while block i is computed.
+    // Blocks of list A (no per-element test) then of list P.
     const int nbA = (cntA + 31) >> 5;
     const int nbt = nbA + ((cntP + 31) >> 5);
-    auto source = [&](int i, const int*& lp, const int*& ll, bool& msk, int& n, int& blk)
-                      __attribute__((always_inline)) {
+    auto source = [&](int i, const int*& lp, bool& msk, int& n, int& blk) __attribute__((always_inline)) {
       msk = i >= nbA;
       lp = msk ? sm.posP : sm.listA;
-      ll = sm.lenP;
       n = msk ? cntP : cntA;
       blk = msk ? i - nbA : i;
     };
-    if (nbt > 0) {
-      {
-        const int* lp;
-        const int* ll;
-        bool msk;
-        int n, blk;
-        source(0, lp, ll, msk, n, blk);
-        issue(lp, n, blk, 0);
-      }
+    const int* lp;
+    bool msk;
+    int n, blk;
+    if (EXACT && nbt > 0) {
+      // Unpipelined: block i + 1 is gathered while block i is computed; buffer
+      // i & 3 is refilled at iteration i + 3, after two more barriers.
+      source(0, lp, msk, n, blk);
+      issue(lp, blk, 0);
       for (int i = 0; i < nbt; ++i) {
-        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's copies have landed
-        __syncthreads();                     // all copies landed; the other buffer is free
-        const int* lp;
-        const int* ll;
-        bool msk;
-        int n, blk;
         if (i + 1 < nbt) {
-          source(i + 1, lp, ll, msk, n, blk);
-          issue(lp, n, blk, (i + 1) & 1);
+          source(i + 1, lp, msk, n, blk);
+          issue(lp, blk, (i + 1) & 3);
         }
-        source(i, lp, ll, msk, n, blk);
-        compute_block(lp, ll, msk, n, blk, i & 1);
+        wait_block(i + 1 < nbt ? 1 : 0);
+        block_barrier();
+        source(i, lp, msk, n, blk);
+        f32x16 x;
+        qk(i & 3, x);
+        prep(x, lp, sm.lenP, msk, n, blk, i & 3);
+        bf16x8 pk[2];
+        softmax(x, pk);
+        VFrag<DB> vf;
+        vfrag_issue(vf, lds_addr(sm.vtile[i & 3] + lane * 4));
+        vfrag_wait(vf);
+        pv(vf, pk);
+      }
+      __syncthreads();
+    } else if (nbt > 0) {
+      // Software pipeline over the blocks. Iteration i computes the scores of
+      // block i + 1 (MFMA) while it turns block i's scores into probabilities
+      // (VALU), then multiplies block i's probabilities with its values. Blocks
+      // i + 2 and i + 3 are being gathered meanwhile; with 4 buffers, the one
+      // refilled at iteration i held block i - 1, finished at iteration i - 1.
+      for (int j = 0; j < 3 && j < nbt; ++j) {
+        source(j, lp, msk, n, blk);
+        issue(lp, blk, j);
+      }
+      wait_block(min(nbt, 3) - 1);
+      block_barrier();
+      f32x16 sc;
+      qk(0, sc);
+      for (int i = 0; i < nbt; ++i) {
+        if (i + 1 < nbt) {
+          wait_block(i + 2 < nbt ? 1 : 0);
+          block_barrier();  // block i + 1 landed everywhere; block i - 1's buffer is free
+        }
+        if (i + 3 < nbt) {
+          source(i + 3, lp, msk, n, blk);
+          issue(lp, blk, (i + 3) & 3);
+        }
+        source(i, lp, msk, n, blk);
+        prep(sc, lp, sm.lenP, msk, n, blk, i & 3);
+        f32x16 sn;
+        qk((i + 1) & 3, sn);  // on the last iteration this reads a stale buffer; unused
+        VFrag<DB> vf;
+        vfrag_issue(vf, lds_addr(sm.vtile[i & 3] + lane * 4));
+        bf16x8 pk[2];
+        softmax(sc, pk);
+        vfrag_wait(vf);
+        pv(vf, pk);
+        sc = sn;
       }
       __syncthreads();
     }
@@ -411,28 +572,22 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
   // Epilogue: combine the two lane halves' sums, normalise, write O (bf16) and LSE.
   // A fast-variant column whose terms overflowed the fixed reference writes NaN to
   // its LSE instead; the exact variant then recomputes the whole tile.
-#pragma unroll
-  for (int c = 0; c < 2; ++c) {
-    float l0, l1;
-    pair_values(l[c], l0, l1);
-    const float lt = l0 + l1;
-    const float inv = lt > 0.f ? 1.0f / lt : 0.f;
-    const bool redo = !EXACT && __builtin_amdgcn_ballot_w64(ovf[c]) != 0;
-    if (qrow[c] >= T) continue;
-    const size_t rowi = ((size_t)b * a.Hq + qh[c]) * T + qrow[c];
+  float l0, l1;
+  pair_values(l, l0, l1);
+  const float lt = l0 + l1;
+  const float inv = lt > 0.f ? 1.0f / lt : 0.f;
+  const bool redo = !EXACT && __builtin_amdgcn_ballot_w64(ovf) != 0;
+  if (qrow < T) {
+    const size_t rowi = ((size_t)b * a.Hq + qh) * T + qrow;
     if (hi == 0)
-      a.lse[rowi] = redo ? __builtin_nanf("") : lt > 0.f ? (m[c] + __builtin_amdgcn_logf(lt)) * kLn2 : -__builtin_inff();
+      a.lse[rowi] = redo ? __builtin_nanf("") : lt > 0.f ? (m + __builtin_amdgcn_logf(lt)) * kLn2 : -__builtin_inff();
     uint16_t* orow = a.o + rowi * D;
 #pragma unroll
     for (int d = 0; d < DB; ++d) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        typedef float f32x4v __attribute__((ext_vector_type(4)));
-        typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-        f32x4v v4 = {o[c][d][4 * g] * inv, o[c][d][4 * g + 1] * inv, o[c][d][4 * g + 2] * inv,
-                     o[c][d][4 * g + 3] * inv};
-        const bf16x4 w4 = __builtin_convertvector(v4, bf16x4);
-        *reinterpret_cast<bf16x4*>(orow + 32 * d + 8 * g + 4 * hi) = w4;
+        const f32x4 v4 = {o[d][4 * g] * inv, o[d][4 * g + 1] * inv, o[d][4 * g + 2] * inv, o[d][4 * g + 3] * inv};
+        *reinterpret_cast<bf16x4*>(orow + 32 * d + 8 * g + 4 * hi) = __builtin_convertvector(v4, bf16x4);
       }
     }
   }
@@ -460,11 +615,14 @@ int launch_hb(const SparseLaunch& L) {
 
 }  // namespace
 
+// Workgroup geometry: 8 (head, 32-query) columns. With G >= 2 a wave pair holds two
+// heads of the same 32 queries; the workgroup covers hc = hpw * nhp heads and a
+// query tile of qt = 32 * (2 / hpw) * wq positions.
 void sparse_attn_plan(SparseLaunch& L) {
   L.G = L.Hq / L.Hkv;
   L.hpw = L.G >= 2 ? 2 : 1;
   const int nhp = L.G / L.hpw < 4 ? L.G / L.hpw : 4;  // head groups per workgroup
-  L.wq = 4 / nhp;                                      // waves along the queries
+  L.wq = 4 / nhp;                                      // wave pairs along the queries
   L.qt = 32 * (2 / L.hpw) * L.wq;
   L.hc = L.hpw * nhp;
   L.nch = L.G / L.hc;
