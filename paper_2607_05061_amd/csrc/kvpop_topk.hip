@@ -15,9 +15,10 @@
 // ..., so cutoff_q is the k-th smallest value of a prefix of the array
 // A_i = rank_{s+i}, which a wavelet matrix over A answers in ceil(log2 T) constant-
 // time steps. One workgroup per sequence builds the ranks (a stable LSD radix sort
-// of 32-bit priority keys, one bit per pass) and the wavelet matrix (one stable
-// partition per bit level, most significant first); then one thread per query
-// walks the levels.
+// of 32-bit priority keys, 8 bits per pass) and the wavelet matrix (one stable
+// partition per bit level, most significant first), moving 1024 consecutive
+// elements per round so that every global access is coalesced; then one thread per
+// query walks the levels.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -80,26 +81,138 @@ __device__ __forceinline__ int block_scan(int v, int* sh, int& total) {
   return excl;
 }
 
-// Stable partition of n (key, val) pairs by bit `bit` of the key: zeros first.
-// Thread t owns the contiguous chunk [t * C, t * C + C). Returns the number of zeros.
-__device__ __forceinline__ int partition_by_bit(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin,
-                                                uint32_t* __restrict__ kout, uint32_t* __restrict__ vout, int n,
-                                                int C, int bit, int* sh) {
-  const int lo = threadIdx.x * C, hi = min(n, lo + C);
-  int zeros = 0;
-  for (int i = lo; i < hi; ++i) zeros += ((kin[i] >> bit) & 1u) == 0u;
-  int ztotal;
-  int zpos = block_scan<false>(zeros, sh, ztotal);
-  int opos = ztotal + (lo - zpos);
-  for (int i = lo; i < hi; ++i) {
-    const uint32_t k = kin[i];
-    const uint32_t v = vout ? vin[i] : 0u;
-    const int dst = ((k >> bit) & 1u) ? opos++ : zpos++;
-    kout[dst] = k;
-    if (vout) vout[dst] = v;
+// LDS of the preparation kernel.
+struct PrepSmem {
+  int cnt[kPrepWaves][256];     // per-wave digit counts of the current round (cleared after use)
+  int pre[kPrepWaves][256];     // destinations: bucket base plus earlier waves of the round
+  int base[256];                // next free slot of each bucket
+  int sh[kPrepWaves + 1];       // block_scan scratch
+  int wc[2][2][kPrepWaves];     // wavelet rounds: [round parity][zeros, ones][wave]
+};
+
+// One stable counting-sort pass on the 8-bit digit at `shift` (a pass of an LSD
+// radix sort). Round r moves elements r * 1024 + tid (coalesced), each to
+// base[d] + (elements of digit d in earlier waves) + (earlier lanes of its wave
+// with digit d), the last found with eight ballots; elements of the next round are
+// loaded while the current one is placed.
+__device__ __forceinline__ void sort_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin,
+                                          uint32_t* __restrict__ kout, uint32_t* __restrict__ vout, int n, int shift,
+                                          PrepSmem& sm) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid < 256) sm.base[tid] = 0;
+  __syncthreads();
+  for (int i = tid; i < n; i += kPrepThreads) atomicAdd(&sm.base[(kin[i] >> shift) & 255u], 1);
+  __syncthreads();
+  int tot;
+  const int ex = block_scan<false>(tid < 256 ? sm.base[tid] : 0, sm.sh, tot);
+  if (tid < 256) sm.base[tid] = ex;
+  __syncthreads();
+  const uint64_t lt = (1ull << lane) - 1ull;
+  uint32_t k = tid < n ? kin[tid] : 0u, v = tid < n ? vin[tid] : 0u;
+  for (int r0 = 0; r0 < n; r0 += kPrepThreads) {
+    const int i = r0 + tid;
+    const bool valid = i < n;
+    const int in = i + kPrepThreads;
+    const uint32_t kn = in < n ? kin[in] : 0u, vn = in < n ? vin[in] : 0u;
+    const int d = (int)((k >> shift) & 255u);
+    uint64_t mm = __builtin_amdgcn_ballot_w64(valid);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const bool bit = (d >> b) & 1;
+      const uint64_t bb = __builtin_amdgcn_ballot_w64(bit);
+      mm &= bit ? bb : ~bb;
+    }
+    const int rk = __popcll(mm & lt);
+    if (valid && rk == 0) sm.cnt[wave][d] = __popcll(mm);
+    __syncthreads();
+    if (tid < 256) {
+      int c[kPrepWaves];
+#pragma unroll
+      for (int w = 0; w < kPrepWaves; ++w) c[w] = sm.cnt[w][tid];
+      int run = sm.base[tid];
+#pragma unroll
+      for (int w = 0; w < kPrepWaves; ++w) {
+        sm.pre[w][tid] = run;
+        sm.cnt[w][tid] = 0;
+        run += c[w];
+      }
+      sm.base[tid] = run;
+    }
+    __syncthreads();
+    if (valid) {
+      const int dst = sm.pre[wave][d] + rk;
+      kout[dst] = k;
+      vout[dst] = v;
+    }
+    k = kn;
+    v = vn;
   }
   __syncthreads();
-  return ztotal;
+}
+
+// One wavelet-matrix level: stable partition of ain by bit `bit` (zeros first) into
+// aout, and the level's bit words bw[W + 1] and ones-before-word counts cw[W + 1].
+// Round r covers elements r * 1024 + tid; each wave's ballot is its 64 bits, i.e.
+// two words of the level.
+__device__ __forceinline__ uint32_t wavelet_level(const uint32_t* __restrict__ ain, uint32_t* __restrict__ aout,
+                                                  int n, int bit, uint32_t* __restrict__ bw,
+                                                  uint32_t* __restrict__ cw, PrepSmem& sm) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int W = (n + 31) / 32;
+  int ones = 0;
+  for (int i = tid; i < n; i += kPrepThreads) ones += (ain[i] >> bit) & 1u;
+  int total_ones;
+  block_scan<false>(ones, sm.sh, total_ones);
+  const uint64_t lt = (1ull << lane) - 1ull;
+  int zrun = 0, orun = n - total_ones;  // next slots of zeros and ones
+  int onesb = 0;                        // ones before this round
+  uint32_t x = tid < n ? ain[tid] : 0u;
+  for (int r0 = 0; r0 < n; r0 += kPrepThreads) {
+    const int i = r0 + tid;
+    const bool valid = i < n;
+    const int in = i + kPrepThreads;
+    const uint32_t xn = in < n ? ain[in] : 0u;
+    const bool one = valid && ((x >> bit) & 1u);
+    const uint64_t ob = __builtin_amdgcn_ballot_w64(one);
+    const uint64_t zb = __builtin_amdgcn_ballot_w64(valid) & ~ob;
+    int* zc = sm.wc[(r0 / kPrepThreads) & 1][0];
+    int* oc = sm.wc[(r0 / kPrepThreads) & 1][1];
+    if (lane == 0) {
+      zc[wave] = __popcll(zb);
+      oc[wave] = __popcll(ob);
+    }
+    __syncthreads();
+    int zpre = 0, opre = 0, ztot = 0, otot = 0;
+#pragma unroll
+    for (int w = 0; w < kPrepWaves; ++w) {
+      const int a = zc[w], b = oc[w];
+      zpre += w < wave ? a : 0;
+      opre += w < wave ? b : 0;
+      ztot += a;
+      otot += b;
+    }
+    if (valid) aout[one ? orun + opre + __popcll(ob & lt) : zrun + zpre + __popcll(zb & lt)] = x;
+    const int p0 = r0 + 64 * wave;
+    if (lane == 0 && p0 < n) {
+      const int wd = p0 >> 5;
+      bw[wd] = (uint32_t)ob;
+      cw[wd] = (uint32_t)(onesb + opre);
+      if (wd + 1 < W) {
+        bw[wd + 1] = (uint32_t)(ob >> 32);
+        cw[wd + 1] = (uint32_t)(onesb + opre + __popc((uint32_t)ob));
+      }
+    }
+    zrun += ztot;
+    orun += otot;
+    onesb += otot;
+    x = xn;
+  }
+  if (tid == 0) {
+    bw[W] = 0u;
+    cw[W] = (uint32_t)total_ones;
+  }
+  __syncthreads();
+  return (uint32_t)(n - total_ones);
 }
 
 struct SegWork {
@@ -136,7 +249,8 @@ __global__ __launch_bounds__(kPrepThreads) void topk_prepare_kernel(const float*
                                                                     const float* __restrict__ log_gamma, int H,
                                                                     int T, int s, int L, void* ws,
                                                                     size_t per_seg_words, int32_t* __restrict__ rank) {
-  __shared__ int sh[kPrepWaves + 1];
+  __shared__ PrepSmem sm;
+  const int tid = threadIdx.x;
   const int seg = blockIdx.x;
   const int h = seg % H;
   SegWork w = seg_work(ws, per_seg_words, seg, T, L);
@@ -145,25 +259,22 @@ __global__ __launch_bounds__(kPrepThreads) void topk_prepare_kernel(const float*
   int32_t* rk = rank + (size_t)seg * T;
   int32_t* ps = w.ps;
 
+  for (int i = tid; i < kPrepWaves * 256; i += kPrepThreads) (&sm.cnt[0][0])[i] = 0;
   // Keys and positions; no fma contraction, to match fl(r - fl(t * lg)).
-  for (int t = threadIdx.x; t < T; t += kPrepThreads) {
-    const float prio = static_priority(r[t], (float)t, lg);
-    w.ka[t] = desc_key(prio);
+  for (int t = tid; t < T; t += kPrepThreads) {
+    w.ka[t] = desc_key(static_priority(r[t], (float)t, lg));
     w.va[t] = (uint32_t)t;
   }
   __syncthreads();
 
-  // Stable LSD radix sort, one bit per pass: equal keys keep position order.
-  const int C = (T + kPrepThreads - 1) / kPrepThreads;
-  uint32_t *kin = w.ka, *kout = w.kb, *vin = w.va, *vout = w.vb;
-  for (int bit = 0; bit < 32; ++bit) {
-    partition_by_bit(kin, vin, kout, vout, T, C, bit, sh);
-    uint32_t* t0 = kin; kin = kout; kout = t0;
-    t0 = vin; vin = vout; vout = t0;
-  }
-  // vin now lists positions by rank.
-  for (int i = threadIdx.x; i < T; i += kPrepThreads) {
-    const int t = (int)vin[i];
+  // Stable LSD radix sort, 8 bits per pass: equal keys keep position order.
+  sort_pass(w.ka, w.va, w.kb, w.vb, T, 0, sm);
+  sort_pass(w.kb, w.vb, w.ka, w.va, T, 8, sm);
+  sort_pass(w.ka, w.va, w.kb, w.vb, T, 16, sm);
+  sort_pass(w.kb, w.vb, w.ka, w.va, T, 24, sm);
+  // va now lists positions by rank.
+  for (int i = tid; i < T; i += kPrepThreads) {
+    const int t = (int)w.va[i];
     ps[i] = t;
     rk[t] = i;
   }
@@ -172,22 +283,17 @@ __global__ __launch_bounds__(kPrepThreads) void topk_prepare_kernel(const float*
   const int n = T - s;  // eligible positions s .. T-1
   if (n <= 0) return;
 
-  // A_i = rank_{s+i}; prefix maxima for the boundary token before saturation.
-  const int Cw = 32 * ((n + 32 * kPrepThreads - 1) / (32 * kPrepThreads));  // whole words per thread
-  {
-    const int lo = threadIdx.x * Cw, hi = min(n, lo + Cw);
-    int m = INT32_MIN;
-    for (int i = lo; i < hi; ++i) {
-      const int a = rk[s + i];
-      w.ka[i] = (uint32_t)a;
-      m = max(m, a);
-    }
+  // A_i = rank_{s+i} and its prefix maxima (the boundary token before saturation),
+  // one coalesced round of 1024 positions at a time.
+  int run = INT32_MIN;
+  for (int r0 = 0; r0 < n; r0 += kPrepThreads) {
+    const int i = r0 + tid;
+    const int av = i < n ? rk[s + i] : INT32_MIN;
+    if (i < n) w.ka[i] = (uint32_t)av;
     int total;
-    int run = block_scan<true>(m, sh, total);
-    for (int i = lo; i < hi; ++i) {
-      run = max(run, (int)w.ka[i]);
-      w.pmax[i] = run;
-    }
+    const int ex = block_scan<true>(av, sm.sh, total);
+    if (i < n) w.pmax[i] = max(run, max(ex, av));
+    run = max(run, total);
   }
   __syncthreads();
 
@@ -195,29 +301,12 @@ __global__ __launch_bounds__(kPrepThreads) void topk_prepare_kernel(const float*
   const int W = (n + 31) / 32;
   uint32_t *ain = w.ka, *aout = w.kb;
   for (int l = 0; l < L; ++l) {
-    const int bit = L - 1 - l;
-    uint32_t* bw = w.bits + (size_t)l * (W + 1);
-    uint32_t* cw = w.cnt + (size_t)l * (W + 1);
-    const int lo = threadIdx.x * Cw, hi = min(n, lo + Cw);
-    int ones = 0;
-    for (int i = lo; i < hi; ++i) ones += (ain[i] >> bit) & 1u;
-    int total_ones;
-    int before = block_scan<false>(ones, sh, total_ones);
-    for (int wd = lo / 32; wd * 32 < hi; ++wd) {
-      uint32_t word = 0;
-      for (int j = 0; j < 32 && wd * 32 + j < hi; ++j) word |= ((ain[wd * 32 + j] >> bit) & 1u) << j;
-      bw[wd] = word;
-      cw[wd] = (uint32_t)before;
-      before += __popc(word);
-    }
-    if (threadIdx.x == 0) {
-      bw[W] = 0u;
-      cw[W] = (uint32_t)total_ones;
-      w.zeros[l] = (uint32_t)(n - total_ones);
-    }
-    __syncthreads();
-    partition_by_bit(ain, nullptr, aout, nullptr, n, Cw, bit, sh);
-    uint32_t* t0 = ain; ain = aout; aout = t0;
+    const uint32_t z = wavelet_level(ain, aout, n, L - 1 - l, w.bits + (size_t)l * (W + 1),
+                                     w.cnt + (size_t)l * (W + 1), sm);
+    if (tid == 0) w.zeros[l] = z;
+    uint32_t* t0 = ain;
+    ain = aout;
+    aout = t0;
   }
 }
 
