@@ -71,6 +71,7 @@ constexpr int kPlane = 512;             // bf16 elements per 1 KB plane
 constexpr int kBufs = 4;                // K/V block buffers (see the block loop)
 constexpr int kChunk = 4096;            // lifetimes staged into LDS per chunk (16 KB)
 constexpr int kEvBufs = 2;              // chunk buffers: the next chunk loads during the scan
+constexpr int kRun = 8;                 // query tiles per workgroup (fast variant)
 
 __device__ __forceinline__ constexpr int acc_row(int r, int hi) { return 8 * (r >> 2) + 4 * hi + (r & 3); }
 
@@ -173,6 +174,7 @@ struct Smem {
   alignas(16) float btile[kBufs][HAS_BIAS ? 64 : 4];
   alignas(16) int evs[kEvBufs][kChunk];  // lifetimes of the positions being scanned
   alignas(16) int listA[kCapA];
+  alignas(16) int eA[kCapA];    // lifetime ends of list A, for the next tile's lists
   alignas(16) int posP[kCapP];  // read 16 bytes at a time
   alignas(16) int lenP[kCapP];
   alignas(16) int scan_sh[2][32];
@@ -184,6 +186,7 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
   using SM = Smem<D, HAS_BIAS>;
   constexpr int KS = SM::KS, DB = SM::DB;
   static_assert(KS == 4 || KS == 8, "head dim 64 or 128");
+  constexpr int RUN = EXACT ? 1 : kRun;  // tiles per workgroup
   __shared__ __attribute__((aligned(16))) SM sm;
 
   const int tid = threadIdx.x;
@@ -191,53 +194,34 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
   const int lane = tid & 63, hi = lane >> 5, col = lane & 31;
   const int T = a.T;
 
-  // Workgroup order. Workgroups are dealt to the 8 XCDs round-robin (XCD =
-  // blockIdx % 8). When the (b, h, chunk) groups divide evenly, each XCD takes its
-  // share of groups one after another, heaviest tile first, so the tiles running
-  // together on an XCD belong to one group and share its keys in that XCD's L2;
-  // otherwise groups interleave within each tile.
+  // Workgroup order. A workgroup takes a run of RUN consecutive query tiles of one
+  // (b, h, chunk) group, in ascending order; runs go heaviest first. Workgroups
+  // are dealt to the 8 XCDs round-robin (XCD = blockIdx % 8): when the groups
+  // divide evenly, each XCD takes its share of groups one after another, so the
+  // tiles running together on an XCD share one group's keys in its L2; otherwise
+  // groups interleave within each run.
   const int groups = a.B * a.Hkv * a.nch;
-  int tile, grp;
+  const int nruns = (a.ntiles + RUN - 1) / RUN;
+  int run, grp;
   if ((groups & 7) == 0) {
     const int x = (int)(blockIdx.x & 7), j = (int)(blockIdx.x >> 3);
-    tile = a.ntiles - 1 - j % a.ntiles;
-    grp = x + 8 * (j / a.ntiles);
+    run = nruns - 1 - j % nruns;
+    grp = x + 8 * (j / nruns);
   } else {
-    tile = a.ntiles - 1 - (int)(blockIdx.x / groups);
+    run = nruns - 1 - (int)(blockIdx.x / groups);
     grp = (int)(blockIdx.x % groups);
   }
   const int bh = grp / a.nch, chunk = grp % a.nch;
   const int b = bh / a.Hkv, h = bh % a.Hkv;
-  const int q0 = tile * a.qt;
-  const int q1 = min(q0 + a.qt, T) - 1;
+  const int tile_end = min(a.ntiles, (run + 1) * RUN);
 
   // This wave's (head, 32-query) column: columns 2 u and 2 u + 1 are two heads of
   // the same queries when G >= 2, two query blocks of one head otherwise.
   const int u = wave >> 1, cc = wave & 1;
   const int hg = u / a.wq, wq = u % a.wq;
   const int qh = h * a.G + chunk * a.hc + hg * HPW + (HPW == 2 ? cc : 0);
-  const int qrow = q0 + 32 * (HPW == 2 ? wq : 2 * wq + cc) + col;
-
-  // The exact variant only redoes tiles the fast variant flagged (NaN in lse).
-  if (EXACT) {
-    const int flagged = qrow < T ? __builtin_isnan(a.lse[((size_t)b * a.Hq + qh) * T + qrow]) : 0;
-    if (!__syncthreads_or(flagged)) return;
-  }
-
-  // Q column in registers as the B operand of S^T = K Q^T: k-step s uses the
-  // 16-byte chunk 2 s + hi of the query row.
-  bf16x8 qf[KS];
-  {
-    const uint16_t* row = a.q + (((size_t)b * a.Hq + qh) * T + min(qrow, T - 1)) * D;
-#pragma unroll
-    for (int s = 0; s < KS; ++s) qf[s] = *reinterpret_cast<const bf16x8*>(row + (2 * s + hi) * 8);
-  }
-
-  f32x16 o[DB];
-#pragma unroll
-  for (int d = 0; d < DB; ++d) o[d] = f32x16{};
-  float m = -__builtin_inff(), l = 0.f;
-  bool ovf = false;
+  const int qcol = 32 * (HPW == 2 ? wq : 2 * wq + cc) + col;  // query offset inside a tile
+  const uint16_t* qbase = a.q + ((size_t)b * a.Hq + qh) * T * D;
 
   const size_t kvoff = (size_t)bh * T * D;
   const int kv_bytes = T * D * 2;
@@ -258,6 +242,13 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
   // V row and column chunk this lane copies into its V plane (layout at pv).
   const int vrow = 16 * (max(vplane, 0) / DB) + 8 * hi + 4 * (col >> 4) + ((lane & 7) >> 1);
   const int vcol_bytes = (16 * ((lane >> 3) & 1) + 8 * (lane & 1)) * 2;
+
+  // State of the current tile, seen by the helpers below.
+  int q0 = 0, q1 = -1, qrow = 0;
+  bf16x8 qf[KS];
+  f32x16 o[DB];
+  float m = 0.f, l = 0.f;
+  bool ovf = false;
 
   // Gather the 32 keys of block `blk` of `lpos` into buffer `buf`. The lists are
   // padded to whole blocks with position -1, which reads as zero rows.
@@ -396,10 +387,11 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
 
   // Lifetimes reach LDS in chunks of kChunk positions, one chunk ahead of the scan,
   // straight from global memory (16 KB per chunk: 2 KB per wave, 2 loads).
-  // Positions past q1 read as 0 (never alive) through the descriptor's range.
-  const __amdgpu_buffer_rsrc_t re =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(ev), (short)0, (q1 + 1) * 4, kRsrcWord3);
+  // Positions past the tile's last query read as 0 (never alive) through the
+  // descriptor's range.
   auto stage = [&](int ch) __attribute__((always_inline)) {
+    const __amdgpu_buffer_rsrc_t re =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(ev), (short)0, (q1 + 1) * 4, kRsrcWord3);
     int* dst = sm.evs[ch & (kEvBufs - 1)];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
@@ -408,197 +400,271 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
                                                (ch * kChunk + idx * 256) * 4, 0, 0);
     }
   };
-  const int last_chunk = q1 / kChunk;
   int staged = 0;  // last chunk whose copies were issued
-  stage(0);
-  int sstep = 0;  // scan steps so far (selects the LDS count buffer)
+  int sstep = 0;   // LDS count exchanges so far (selects the buffer)
 
-  // Windows of key positions [w0, w1): the compaction scan over their lifetimes
-  // stops before either list could overflow, and the window's lists are then
-  // processed in full. With the running top-k policy one window covers 0 .. q1.
-  // (Scanning first and computing after keeps the accumulators in one place; a
-  // scan interleaved with the block loop makes the compiler copy them.)
-  for (int w0 = 0; w0 <= q1;) {
-    int cntA = 0, cntP = 0;
-    int base = w0;
-    while (base <= q1 && cntA <= kCapA - kScan && cntP <= kCapP - kScan) {
-      if ((base & (kChunk - 1)) == 0) {
-        // This chunk has landed once only the next chunk's copies (2 per wave,
-        // issued after it; loads complete in order) are outstanding.
-        const int c = base / kChunk;
-        if (staged > c) wait_vmcnt<2>();
-        else wait_vmcnt<0>();
-        block_barrier();  // for every wave; chunk c - 1's buffer is free
-        if (c + 1 <= last_chunk) stage(staged = c + 1);
-      }
-      // Thread tid looks at positions base + 512 j + tid, so each wave's ballot is
-      // already in position order; wave counts are exchanged once through LDS.
-      const int* evc = sm.evs[(base / kChunk) & (kEvBufs - 1)] + (base & (kChunk - 1));
-      uint64_t bf[2], bp[2];
-      int len[2];
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int p = base + 512 * j + tid;
-        const int e = p <= q1 ? evc[512 * j + tid] : 0;
-        const bool alive = p <= q1 && e > max(p, q0);  // kept by some query of the tile
-        const bool full = alive && p <= q0 && e > q1;   // kept by all of them
-        bf[j] = __builtin_amdgcn_ballot_w64(full);
-        bp[j] = __builtin_amdgcn_ballot_w64(alive && !full);
-        len[j] = e - p;
-      }
-      int* sh = sm.scan_sh[sstep & 1];  // [kind][j][wave]
-      if (lane == 0) {
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          sh[j * 8 + wave] = __builtin_popcountll(bf[j]);
-          sh[16 + j * 8 + wave] = __builtin_popcountll(bp[j]);
-        }
-      }
-      lds_sync();
-      int ia = cntA, ip = cntP;
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        int befA = 0, befP = 0, totA = 0, totP = 0;
-#pragma unroll
-        for (int w = 0; w < kWaves; ++w) {
-          const int ca = sh[j * 8 + w], cp = sh[16 + j * 8 + w];
-          befA += w < wave ? ca : 0;
-          befP += w < wave ? cp : 0;
-          totA += ca;
-          totP += cp;
-        }
-        const int p = base + 512 * j + tid;
-        const int ra = __builtin_amdgcn_mbcnt_hi((uint32_t)(bf[j] >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bf[j], 0));
-        const int rp = __builtin_amdgcn_mbcnt_hi((uint32_t)(bp[j] >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bp[j], 0));
-        if ((bf[j] >> lane) & 1) sm.listA[ia + befA + ra] = p;
-        if ((bp[j] >> lane) & 1) {
-          sm.posP[ip + befP + rp] = p;
-          sm.lenP[ip + befP + rp] = len[j];
-        }
-        ia += totA;
-        ip += totP;
-      }
-      cntA = ia;
-      cntP = ip;
-      ++sstep;
-      base += kScan;
+  // Append one candidate key per thread (t with lifetime end e; `valid` false for
+  // none) to lists A and P of the current tile, in thread order after the nA / nP
+  // entries already there. Returns false, leaving the lists unusable, if either
+  // list would overflow.
+  auto append = [&](bool valid, int t, int e, int& nA, int& nP) __attribute__((always_inline)) {
+    const bool alive = valid && e > max(t, q0);  // kept by some query of the tile
+    const bool full = alive && t <= q0 && e > q1;  // kept by all of them
+    const uint64_t bf = __builtin_amdgcn_ballot_w64(full);
+    const uint64_t bp = __builtin_amdgcn_ballot_w64(alive && !full);
+    int* sh = sm.scan_sh[sstep & 1];
+    if (lane == 0) {
+      sh[wave] = __builtin_popcountll(bf);
+      sh[16 + wave] = __builtin_popcountll(bp);
     }
-    // Pad both lists to whole blocks: position -1 (zero rows), lifetime 0.
-    if (tid < 32) {
-      if (cntA + tid < ((cntA + 31) & ~31)) sm.listA[cntA + tid] = -1;
-      if (cntP + tid < ((cntP + 31) & ~31)) {
-        sm.posP[cntP + tid] = -1;
-        sm.lenP[cntP + tid] = 0;
-      }
+    lds_sync();
+    int befA = 0, befP = 0, totA = 0, totP = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const int ca = sh[w], cp = sh[16 + w];
+      befA += w < wave ? ca : 0;
+      befP += w < wave ? cp : 0;
+      totA += ca;
+      totP += cp;
     }
-    lds_sync();  // the lists are complete and visible to every wave
-    w0 = base;
+    const bool fits = nA + totA <= kCapA && nP + totP <= kCapP;
+    if (fits && full) {
+      const int i = nA + befA + __builtin_amdgcn_mbcnt_hi((uint32_t)(bf >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bf, 0));
+      sm.listA[i] = t;
+      sm.eA[i] = e;
+    }
+    if (fits && alive && !full) {
+      const int i = nP + befP + __builtin_amdgcn_mbcnt_hi((uint32_t)(bp >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bp, 0));
+      sm.posP[i] = t;
+      sm.lenP[i] = e - t;
+    }
+    nA += totA;
+    nP += totP;
+    ++sstep;
+    return fits;
+  };
 
-    // Blocks of list A (no per-element test) then of list P.
-    const int nbA = (cntA + 31) >> 5;
-    const int nbt = nbA + ((cntP + 31) >> 5);
-    auto source = [&](int i, const int*& lp, bool& msk, int& n, int& blk) __attribute__((always_inline)) {
-      msk = i >= nbA;
-      lp = msk ? sm.posP : sm.listA;
-      n = msk ? cntP : cntA;
-      blk = msk ? i - nbA : i;
-    };
-    const int* lp;
-    bool msk;
-    int n, blk;
-    if (EXACT && nbt > 0) {
-      // Unpipelined: block i + 1 is gathered while block i is computed; buffer
-      // i & 3 is refilled at iteration i + 3, after two more barriers.
-      source(0, lp, msk, n, blk);
-      issue(lp, blk, 0);
-      for (int i = 0; i < nbt; ++i) {
-        if (i + 1 < nbt) {
-          source(i + 1, lp, msk, n, blk);
-          issue(lp, blk, (i + 1) & 3);
+  int cntA = 0, cntP = 0;  // list sizes (without padding)
+  bool lists_ok = false;   // the lists hold every key of the previous tile
+
+  for (int tile = run * RUN; tile < tile_end; ++tile) {
+    const int pq1 = q1;
+    q0 = tile * a.qt;
+    q1 = min(q0 + a.qt, T) - 1;
+    qrow = q0 + qcol;
+
+    // The exact variant only redoes tiles the fast variant flagged (NaN in lse).
+    if (EXACT) {
+      const int flagged = qrow < T ? __builtin_isnan(a.lse[((size_t)b * a.Hq + qh) * T + qrow]) : 0;
+      if (!__syncthreads_or(flagged)) return;
+    }
+
+    // Q column in registers as the B operand of S^T = K Q^T: k-step s uses the
+    // 16-byte chunk 2 s + hi of the query row.
+    {
+      const uint16_t* row = qbase + (size_t)min(qrow, T - 1) * D;
+#pragma unroll
+      for (int s = 0; s < KS; ++s) qf[s] = *reinterpret_cast<const bf16x8*>(row + (2 * s + hi) * 8);
+    }
+#pragma unroll
+    for (int d = 0; d < DB; ++d) o[d] = f32x16{};
+    m = -__builtin_inff();
+    l = 0.f;
+    ovf = false;
+
+    // Lists of the tile from the previous tile's (its keys still alive, reclassified,
+    // plus the new positions pq1 + 1 .. q1), or from a full scan.
+    bool have = false;
+    if (lists_ok) {
+      int pt[kCapP / kThreads], pe[kCapP / kThreads];  // list P moves to registers first
+#pragma unroll
+      for (int k = 0; k < kCapP / kThreads; ++k) {
+        const int i = tid + k * kThreads;
+        pt[k] = i < cntP ? sm.posP[i] : 0;
+        pe[k] = i < cntP ? sm.posP[i] + sm.lenP[i] : 0;
+      }
+      int nA = 0, nP = 0;
+      bool fits = true;
+      // List A in place, 512 entries at a time: an entry's new index never exceeds
+      // its old one, and every thread reads its entry before append's barrier.
+      for (int c0 = 0; c0 < cntA; c0 += kThreads) {
+        const int i = c0 + tid;
+        const bool v = i < cntA;
+        const int t = v ? sm.listA[i] : 0, e = v ? sm.eA[i] : 0;
+        fits = append(v, t, e, nA, nP) && fits;
+      }
+#pragma unroll
+      for (int k = 0; k < kCapP / kThreads; ++k)
+        if (k * kThreads < cntP) fits = append(tid + k * kThreads < cntP, pt[k], pe[k], nA, nP) && fits;
+      {
+        const int p = pq1 + 1 + tid;
+        const bool v = p <= q1;
+        fits = append(v, p, v ? ev[p] : 0, nA, nP) && fits;
+      }
+      have = fits;
+      cntA = nA;
+      cntP = nP;
+    }
+
+    // Windows of key positions [w0, w1): the compaction scan over their lifetimes
+    // stops before either list could overflow, and the window's lists are then
+    // processed in full. With the running top-k policy one window covers 0 .. q1.
+    // (Scanning first and computing after keeps the accumulators in one place; a
+    // scan interleaved with the block loop makes the compiler copy them.)
+    lists_ok = true;
+    for (int w0 = 0, first = 1; w0 <= q1; first = 0) {
+      if (have) {
+        w0 = q1 + 1;
+      } else {
+        if (w0 == 0) {
+          stage(0);
+          staged = 0;
         }
-        wait_block(i + 1 < nbt ? 1 : 0);
+        const int last_chunk = q1 / kChunk;
+        cntA = 0;
+        cntP = 0;
+        int base = w0;
+        while (base <= q1 && cntA <= kCapA - kScan && cntP <= kCapP - kScan) {
+          if ((base & (kChunk - 1)) == 0) {
+            // This chunk has landed once only the next chunk's copies (2 per wave,
+            // issued after it; loads complete in order) are outstanding.
+            const int c = base / kChunk;
+            if (staged > c) wait_vmcnt<2>();
+            else wait_vmcnt<0>();
+            block_barrier();  // for every wave; chunk c - 1's buffer is free
+            if (c + 1 <= last_chunk) stage(staged = c + 1);
+          }
+          // Thread tid looks at positions base + 512 j + tid, so each wave's ballot
+          // is already in position order.
+          const int* evc = sm.evs[(base / kChunk) & (kEvBufs - 1)] + (base & (kChunk - 1));
+#pragma unroll
+          for (int j = 0; j < 2; ++j) {
+            const int p = base + 512 * j + tid;
+            append(p <= q1, p, p <= q1 ? evc[512 * j + tid] : 0, cntA, cntP);
+          }
+          base += kScan;
+        }
+        lists_ok = lists_ok && first && base > q1;  // one window: the lists are complete
+        w0 = base;
+      }
+      // Pad both lists to whole blocks: position -1 (zero rows), lifetime 0.
+      if (tid < 32) {
+        if (cntA + tid < ((cntA + 31) & ~31)) sm.listA[cntA + tid] = -1;
+        if (cntP + tid < ((cntP + 31) & ~31)) {
+          sm.posP[cntP + tid] = -1;
+          sm.lenP[cntP + tid] = 0;
+        }
+      }
+      lds_sync();  // the lists are complete and visible to every wave
+
+      // Blocks of list A (no per-element test) then of list P.
+      const int nbA = (cntA + 31) >> 5;
+      const int nbt = nbA + ((cntP + 31) >> 5);
+      auto source = [&](int i, const int*& lp, bool& msk, int& n, int& blk) __attribute__((always_inline)) {
+        msk = i >= nbA;
+        lp = msk ? sm.posP : sm.listA;
+        n = msk ? cntP : cntA;
+        blk = msk ? i - nbA : i;
+      };
+      const int* lp;
+      bool msk;
+      int n, blk;
+      if (EXACT && nbt > 0) {
+        // Unpipelined: block i + 1 is gathered while block i is computed; buffer
+        // i & 3 is refilled at iteration i + 3, after two more barriers.
+        source(0, lp, msk, n, blk);
+        issue(lp, blk, 0);
+        for (int i = 0; i < nbt; ++i) {
+          if (i + 1 < nbt) {
+            source(i + 1, lp, msk, n, blk);
+            issue(lp, blk, (i + 1) & 3);
+          }
+          wait_block(i + 1 < nbt ? 1 : 0);
+          block_barrier();
+          source(i, lp, msk, n, blk);
+          f32x16 x;
+          qk(i & 3, x);
+          prep(x, lp, sm.lenP, msk, n, blk, i & 3);
+          bf16x8 pk[2];
+          softmax(x, pk);
+          VFrag<DB> vf;
+          vfrag_issue(vf, lds_addr(sm.vtile[i & 3] + lane * 4));
+          vfrag_wait(vf);
+          pv(vf, pk);
+        }
+        __syncthreads();
+      } else if (nbt > 0) {
+        // Software pipeline over the blocks. Iteration i computes the scores of
+        // block i + 1 (MFMA) while it turns block i's scores into probabilities
+        // (VALU), then multiplies block i's probabilities with its values. Blocks
+        // i + 2 and i + 3 are being gathered meanwhile; with 4 buffers, the one
+        // refilled at iteration i held block i - 1, finished at iteration i - 1.
+        for (int j = 0; j < 3 && j < nbt; ++j) {
+          source(j, lp, msk, n, blk);
+          issue(lp, blk, j);
+        }
+        wait_block(min(nbt, 3) - 1);
         block_barrier();
-        source(i, lp, msk, n, blk);
-        f32x16 x;
-        qk(i & 3, x);
-        prep(x, lp, sm.lenP, msk, n, blk, i & 3);
-        bf16x8 pk[2];
-        softmax(x, pk);
-        VFrag<DB> vf;
-        vfrag_issue(vf, lds_addr(sm.vtile[i & 3] + lane * 4));
-        vfrag_wait(vf);
-        pv(vf, pk);
-      }
-      __syncthreads();
-    } else if (nbt > 0) {
-      // Software pipeline over the blocks. Iteration i computes the scores of
-      // block i + 1 (MFMA) while it turns block i's scores into probabilities
-      // (VALU), then multiplies block i's probabilities with its values. Blocks
-      // i + 2 and i + 3 are being gathered meanwhile; with 4 buffers, the one
-      // refilled at iteration i held block i - 1, finished at iteration i - 1.
-      for (int j = 0; j < 3 && j < nbt; ++j) {
-        source(j, lp, msk, n, blk);
-        issue(lp, blk, j);
-      }
-      wait_block(min(nbt, 3) - 1);
-      block_barrier();
-      f32x16 sc;
-      qk(0, sc);
-      for (int i = 0; i < nbt; ++i) {
-        if (i + 1 < nbt) {
-          wait_block(i + 2 < nbt ? 1 : 0);
-          block_barrier();  // block i + 1 landed everywhere; block i - 1's buffer is free
+        f32x16 sc;
+        qk(0, sc);
+        for (int i = 0; i < nbt; ++i) {
+          if (i + 1 < nbt) {
+            wait_block(i + 2 < nbt ? 1 : 0);
+            block_barrier();  // block i + 1 landed everywhere; block i - 1's buffer is free
+          }
+          if (i + 3 < nbt) {
+            source(i + 3, lp, msk, n, blk);
+            issue(lp, blk, (i + 3) & 3);
+          }
+          source(i, lp, msk, n, blk);
+          prep(sc, lp, sm.lenP, msk, n, blk, i & 3);
+          f32x16 sn;
+          qk((i + 1) & 3, sn);  // on the last iteration this reads a stale buffer; unused
+          VFrag<DB> vf;
+          vfrag_issue(vf, lds_addr(sm.vtile[i & 3] + lane * 4));
+          bf16x8 pk[2];
+          softmax(sc, pk);
+          vfrag_wait(vf);
+          pv(vf, pk);
+          sc = sn;
         }
-        if (i + 3 < nbt) {
-          source(i + 3, lp, msk, n, blk);
-          issue(lp, blk, (i + 3) & 3);
-        }
-        source(i, lp, msk, n, blk);
-        prep(sc, lp, sm.lenP, msk, n, blk, i & 3);
-        f32x16 sn;
-        qk((i + 1) & 3, sn);  // on the last iteration this reads a stale buffer; unused
-        VFrag<DB> vf;
-        vfrag_issue(vf, lds_addr(sm.vtile[i & 3] + lane * 4));
-        bf16x8 pk[2];
-        softmax(sc, pk);
-        vfrag_wait(vf);
-        pv(vf, pk);
-        sc = sn;
+        __syncthreads();
       }
-      __syncthreads();
     }
-  }
 
-  // Epilogue: combine the two lane halves' sums, normalise, write O (bf16) and LSE.
-  // A fast-variant column whose terms overflowed the fixed reference writes NaN to
-  // its LSE instead; the exact variant then recomputes the whole tile.
-  float l0, l1;
-  pair_values(l, l0, l1);
-  const float lt = l0 + l1;
-  const float inv = lt > 0.f ? 1.0f / lt : 0.f;
-  const bool redo = !EXACT && __builtin_amdgcn_ballot_w64(ovf) != 0;
-  if (qrow < T) {
-    const size_t rowi = ((size_t)b * a.Hq + qh) * T + qrow;
-    if (hi == 0)
-      a.lse[rowi] = redo ? __builtin_nanf("") : lt > 0.f ? (m + __builtin_amdgcn_logf(lt)) * kLn2 : -__builtin_inff();
-    uint16_t* orow = a.o + rowi * D;
+    // Epilogue: combine the two lane halves' sums, normalise, write O (bf16) and
+    // LSE. A fast-variant column whose terms overflowed the fixed reference writes
+    // NaN to its LSE instead; the exact variant then recomputes the whole tile.
+    float l0, l1;
+    pair_values(l, l0, l1);
+    const float lt = l0 + l1;
+    const float inv = lt > 0.f ? 1.0f / lt : 0.f;
+    const bool redo = !EXACT && __builtin_amdgcn_ballot_w64(ovf) != 0;
+    if (qrow < T) {
+      const size_t rowi = ((size_t)b * a.Hq + qh) * T + qrow;
+      if (hi == 0)
+        a.lse[rowi] = redo ? __builtin_nanf("") : lt > 0.f ? (m + __builtin_amdgcn_logf(lt)) * kLn2 : -__builtin_inff();
+      uint16_t* orow = a.o + rowi * D;
 #pragma unroll
-    for (int d = 0; d < DB; ++d) {
+      for (int d = 0; d < DB; ++d) {
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const f32x4 v4 = {o[d][4 * g] * inv, o[d][4 * g + 1] * inv, o[d][4 * g + 2] * inv, o[d][4 * g + 3] * inv};
-        *reinterpret_cast<bf16x4*>(orow + 32 * d + 8 * g + 4 * hi) = __builtin_convertvector(v4, bf16x4);
+        for (int g = 0; g < 4; ++g) {
+          const f32x4 v4 = {o[d][4 * g] * inv, o[d][4 * g + 1] * inv, o[d][4 * g + 2] * inv, o[d][4 * g + 3] * inv};
+          *reinterpret_cast<bf16x4*>(orow + 32 * d + 8 * g + 4 * hi) = __builtin_convertvector(v4, bf16x4);
+        }
       }
     }
   }
 }
 
-// The fast variant, then the exact one, which exits at once on tiles the fast one
-// did not flag.
+// The fast variant (runs of kRun tiles per workgroup), then the exact one (one tile
+// per workgroup), which exits at once on tiles the fast one did not flag.
 template <int D, int HPW, bool HB>
 int launch_d(const SparseLaunch& L) {
-  const unsigned grid = (unsigned)((long long)L.ntiles * L.B * L.Hkv * L.nch);
-  hipLaunchKernelGGL((sparse_attn_fwd_kernel<D, HPW, HB, false>), dim3(grid), dim3(kThreads), 0,
+  const unsigned groups = (unsigned)(L.B * L.Hkv * L.nch);
+  const unsigned grid_fast = (unsigned)((L.ntiles + kRun - 1) / kRun) * groups;
+  const unsigned grid = (unsigned)L.ntiles * groups;
+  hipLaunchKernelGGL((sparse_attn_fwd_kernel<D, HPW, HB, false>), dim3(grid_fast), dim3(kThreads), 0,
                      (hipStream_t)L.stream, L);
   int e = (int)hipGetLastError();
   if (e) return e;
