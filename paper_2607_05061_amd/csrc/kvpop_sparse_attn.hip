@@ -164,6 +164,42 @@ __device__ __forceinline__ void vfrag_wait(VFrag<2>& f) {
                  "+v"(f.r[7]));
 }
 
+// The K fragments of a block (the A operands of S^T = K Q^T: k-step s at byte
+// 1024 s + 16 lane of the K tile), read from inline asm for the same reason.
+template <int KS>
+struct KFrag {
+  bf16x8 r[KS];
+};
+
+__device__ __forceinline__ void kfrag_issue(KFrag<8>& f, uint32_t a) {
+  asm volatile(
+      "ds_read_b128 %0, %8 offset:0\n ds_read_b128 %1, %8 offset:1024\n"
+      "ds_read_b128 %2, %8 offset:2048\n ds_read_b128 %3, %8 offset:3072\n"
+      "ds_read_b128 %4, %8 offset:4096\n ds_read_b128 %5, %8 offset:5120\n"
+      "ds_read_b128 %6, %8 offset:6144\n ds_read_b128 %7, %8 offset:7168"
+      : "=&v"(f.r[0]), "=&v"(f.r[1]), "=&v"(f.r[2]), "=&v"(f.r[3]), "=&v"(f.r[4]), "=&v"(f.r[5]), "=&v"(f.r[6]),
+        "=&v"(f.r[7])
+      : "v"(a));
+}
+
+__device__ __forceinline__ void kfrag_wait(KFrag<8>& f) {
+  asm volatile("s_waitcnt lgkmcnt(0)"
+               : "+v"(f.r[0]), "+v"(f.r[1]), "+v"(f.r[2]), "+v"(f.r[3]), "+v"(f.r[4]), "+v"(f.r[5]), "+v"(f.r[6]),
+                 "+v"(f.r[7]));
+}
+
+__device__ __forceinline__ void kfrag_issue(KFrag<4>& f, uint32_t a) {
+  asm volatile(
+      "ds_read_b128 %0, %4 offset:0\n ds_read_b128 %1, %4 offset:1024\n"
+      "ds_read_b128 %2, %4 offset:2048\n ds_read_b128 %3, %4 offset:3072"
+      : "=&v"(f.r[0]), "=&v"(f.r[1]), "=&v"(f.r[2]), "=&v"(f.r[3])
+      : "v"(a));
+}
+
+__device__ __forceinline__ void kfrag_wait(KFrag<4>& f) {
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(f.r[0]), "+v"(f.r[1]), "+v"(f.r[2]), "+v"(f.r[3]));
+}
+
 template <int D, bool HAS_BIAS>
 struct Smem {
   static constexpr int KS = D / 16;  // K planes per block (k-steps over the head dim)
@@ -293,6 +329,13 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
 #pragma unroll
     for (int s = 0; s < KS; ++s)
       sacc = mfma32(*reinterpret_cast<const bf16x8*>(kt + s * kPlane + lane * 8), qf[s], sacc);
+  };
+
+  // The same product from fragments read by kfrag_issue.
+  auto qk_regs = [&](const KFrag<KS>& f, f32x16& sacc) __attribute__((always_inline)) {
+    sacc = f32x16{};
+#pragma unroll
+    for (int s = 0; s < KS; ++s) sacc = mfma32(f.r[s], qf[s], sacc);
   };
 
   // Key bias and masking of block `blk` of a list (entries lpos/llen, n of them):
@@ -616,12 +659,18 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
             source(i + 3, lp, msk, n, blk);
             issue(lp, blk, (i + 3) & 3);
           }
-          source(i, lp, msk, n, blk);
-          prep(sc, lp, sm.lenP, msk, n, blk, i & 3);
-          f32x16 sn;
-          qk((i + 1) & 3, sn);  // on the last iteration this reads a stale buffer; unused
+          // Block i + 1's K fragments (on the last iteration a stale buffer; the
+          // scores are unused) and block i's V fragments, read without the compiler's
+          // waits for the copies in flight.
+          KFrag<KS> kf;
+          kfrag_issue(kf, lds_addr(sm.ktile[(i + 1) & 3] + lane * 8));
           VFrag<DB> vf;
           vfrag_issue(vf, lds_addr(sm.vtile[i & 3] + lane * 4));
+          source(i, lp, msk, n, blk);
+          prep(sc, lp, sm.lenP, msk, n, blk, i & 3);
+          kfrag_wait(kf);
+          f32x16 sn;
+          qk_regs(kf, sn);
           bf16x8 pk[2];
           softmax(sc, pk);
           vfrag_wait(vf);
