@@ -82,19 +82,22 @@ __device__ __forceinline__ int block_scan(int v, int* sh, int& total) {
 }
 
 // LDS of the preparation kernel.
+constexpr int kSortJ = 4;  // elements per thread in a sort round
+
 struct PrepSmem {
-  int cnt[kPrepWaves][256];     // per-wave digit counts of the current round (cleared after use)
-  int pre[kPrepWaves][256];     // destinations: bucket base plus earlier waves of the round
+  int cnt[kSortJ][kPrepWaves][256];  // per-(slot, wave) digit counts of a round (cleared after use)
+  int pre[kSortJ][kPrepWaves][256];  // destinations: bucket base plus earlier (slot, wave)s
   int base[256];                // next free slot of each bucket
   int sh[kPrepWaves + 1];       // block_scan scratch
-  int wc[2][2][kPrepWaves];     // wavelet rounds: [round parity][zeros, ones][wave]
+  int wc[2][2][4 * kPrepWaves]; // wavelet rounds: [round parity][zeros, ones][j * 16 + wave]
+  int bitcnt[32];               // elements of A with each bit set
 };
 
 // One stable counting-sort pass on the 8-bit digit at `shift` (a pass of an LSD
-// radix sort). Round r moves elements r * 1024 + tid (coalesced), each to
-// base[d] + (elements of digit d in earlier waves) + (earlier lanes of its wave
-// with digit d), the last found with eight ballots; elements of the next round are
-// loaded while the current one is placed.
+// radix sort). A round moves 4096 elements: thread tid takes r0 + 1024 j + tid for
+// j = 0..3, each placed at base[d] + (elements of digit d in earlier (j, wave)
+// pairs of the round) + (earlier lanes of its wave with digit d), the last found
+// with eight ballots.
 __device__ __forceinline__ void sort_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin,
                                           uint32_t* __restrict__ kout, uint32_t* __restrict__ vout, int n, int shift,
                                           PrepSmem& sm) {
@@ -108,104 +111,131 @@ __device__ __forceinline__ void sort_pass(const uint32_t* __restrict__ kin, cons
   if (tid < 256) sm.base[tid] = ex;
   __syncthreads();
   const uint64_t lt = (1ull << lane) - 1ull;
-  uint32_t k = tid < n ? kin[tid] : 0u, v = tid < n ? vin[tid] : 0u;
-  for (int r0 = 0; r0 < n; r0 += kPrepThreads) {
-    const int i = r0 + tid;
-    const bool valid = i < n;
-    const int in = i + kPrepThreads;
-    const uint32_t kn = in < n ? kin[in] : 0u, vn = in < n ? vin[in] : 0u;
-    const int d = (int)((k >> shift) & 255u);
-    uint64_t mm = __builtin_amdgcn_ballot_w64(valid);
+  for (int r0 = 0; r0 < n; r0 += kSortJ * kPrepThreads) {
+    uint32_t k[kSortJ], v[kSortJ];
+    int d[kSortJ], rk[kSortJ];
+    bool valid[kSortJ];
 #pragma unroll
-    for (int b = 0; b < 8; ++b) {
-      const bool bit = (d >> b) & 1;
-      const uint64_t bb = __builtin_amdgcn_ballot_w64(bit);
-      mm &= bit ? bb : ~bb;
+    for (int j = 0; j < kSortJ; ++j) {
+      const int i = r0 + 1024 * j + tid;
+      valid[j] = i < n;
+      k[j] = valid[j] ? kin[i] : 0u;
+      v[j] = valid[j] ? vin[i] : 0u;
     }
-    const int rk = __popcll(mm & lt);
-    if (valid && rk == 0) sm.cnt[wave][d] = __popcll(mm);
+#pragma unroll
+    for (int j = 0; j < kSortJ; ++j) {
+      d[j] = (int)((k[j] >> shift) & 255u);
+      uint64_t mm = __builtin_amdgcn_ballot_w64(valid[j]);
+#pragma unroll
+      for (int b = 0; b < 8; ++b) {
+        const bool bit = (d[j] >> b) & 1;
+        const uint64_t bb = __builtin_amdgcn_ballot_w64(bit);
+        mm &= bit ? bb : ~bb;
+      }
+      rk[j] = __popcll(mm & lt);
+      if (valid[j] && rk[j] == 0) sm.cnt[j][wave][d[j]] = __popcll(mm);
+    }
     __syncthreads();
     if (tid < 256) {
-      int c[kPrepWaves];
-#pragma unroll
-      for (int w = 0; w < kPrepWaves; ++w) c[w] = sm.cnt[w][tid];
       int run = sm.base[tid];
 #pragma unroll
-      for (int w = 0; w < kPrepWaves; ++w) {
-        sm.pre[w][tid] = run;
-        sm.cnt[w][tid] = 0;
-        run += c[w];
+      for (int j = 0; j < kSortJ; ++j) {
+        int c[kPrepWaves];
+#pragma unroll
+        for (int w = 0; w < kPrepWaves; ++w) c[w] = sm.cnt[j][w][tid];
+#pragma unroll
+        for (int w = 0; w < kPrepWaves; ++w) {
+          sm.pre[j][w][tid] = run;
+          sm.cnt[j][w][tid] = 0;
+          run += c[w];
+        }
       }
       sm.base[tid] = run;
     }
     __syncthreads();
-    if (valid) {
-      const int dst = sm.pre[wave][d] + rk;
-      kout[dst] = k;
-      vout[dst] = v;
+#pragma unroll
+    for (int j = 0; j < kSortJ; ++j) {
+      if (valid[j]) {
+        const int dst = sm.pre[j][wave][d[j]] + rk[j];
+        kout[dst] = k[j];
+        vout[dst] = v[j];
+      }
     }
-    k = kn;
-    v = vn;
   }
   __syncthreads();
 }
 
 // One wavelet-matrix level: stable partition of ain by bit `bit` (zeros first) into
 // aout, and the level's bit words bw[W + 1] and ones-before-word counts cw[W + 1].
-// Round r covers elements r * 1024 + tid; each wave's ballot is its 64 bits, i.e.
-// two words of the level.
+// A round covers 4096 elements: thread tid takes r0 + 1024 j + tid for j = 0..3, so
+// each (j, wave) ballot is 64 consecutive bits, i.e. two words of the level; the
+// zeros and ones before each (j, wave) come from one exchange of the 64 counts and a
+// scan across the lanes of every wave.
+// total_ones: elements with bit `bit` set (a reordering does not change it).
 __device__ __forceinline__ uint32_t wavelet_level(const uint32_t* __restrict__ ain, uint32_t* __restrict__ aout,
-                                                  int n, int bit, uint32_t* __restrict__ bw,
+                                                  int n, int bit, int total_ones, uint32_t* __restrict__ bw,
                                                   uint32_t* __restrict__ cw, PrepSmem& sm) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int W = (n + 31) / 32;
-  int ones = 0;
-  for (int i = tid; i < n; i += kPrepThreads) ones += (ain[i] >> bit) & 1u;
-  int total_ones;
-  block_scan<false>(ones, sm.sh, total_ones);
   const uint64_t lt = (1ull << lane) - 1ull;
   int zrun = 0, orun = n - total_ones;  // next slots of zeros and ones
   int onesb = 0;                        // ones before this round
-  uint32_t x = tid < n ? ain[tid] : 0u;
-  for (int r0 = 0; r0 < n; r0 += kPrepThreads) {
-    const int i = r0 + tid;
-    const bool valid = i < n;
-    const int in = i + kPrepThreads;
-    const uint32_t xn = in < n ? ain[in] : 0u;
-    const bool one = valid && ((x >> bit) & 1u);
-    const uint64_t ob = __builtin_amdgcn_ballot_w64(one);
-    const uint64_t zb = __builtin_amdgcn_ballot_w64(valid) & ~ob;
-    int* zc = sm.wc[(r0 / kPrepThreads) & 1][0];
-    int* oc = sm.wc[(r0 / kPrepThreads) & 1][1];
+  for (int r0 = 0, par = 0; r0 < n; r0 += 4 * kPrepThreads, par ^= 1) {
+    uint32_t x[4];
+    bool one[4], valid[4];
+    uint64_t ob[4], zb[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = r0 + 1024 * j + tid;
+      valid[j] = i < n;
+      x[j] = valid[j] ? ain[i] : 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      one[j] = valid[j] && ((x[j] >> bit) & 1u);
+      ob[j] = __builtin_amdgcn_ballot_w64(one[j]);
+      zb[j] = __builtin_amdgcn_ballot_w64(valid[j]) & ~ob[j];
+    }
+    int* zc = sm.wc[par][0];  // [j * 16 + wave]
+    int* oc = sm.wc[par][1];
     if (lane == 0) {
-      zc[wave] = __popcll(zb);
-      oc[wave] = __popcll(ob);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        zc[j * kPrepWaves + wave] = __popcll(zb[j]);
+        oc[j * kPrepWaves + wave] = __popcll(ob[j]);
+      }
     }
     __syncthreads();
-    int zpre = 0, opre = 0, ztot = 0, otot = 0;
+    // Exclusive scans of the 64 counts in (j, wave) order, one count per lane.
+    int zi = zc[lane], oi = oc[lane];
 #pragma unroll
-    for (int w = 0; w < kPrepWaves; ++w) {
-      const int a = zc[w], b = oc[w];
-      zpre += w < wave ? a : 0;
-      opre += w < wave ? b : 0;
-      ztot += a;
-      otot += b;
+    for (int off = 1; off < 64; off <<= 1) {
+      const int zy = __shfl_up(zi, off), oy = __shfl_up(oi, off);
+      if (lane >= off) {
+        zi += zy;
+        oi += oy;
+      }
     }
-    if (valid) aout[one ? orun + opre + __popcll(ob & lt) : zrun + zpre + __popcll(zb & lt)] = x;
-    const int p0 = r0 + 64 * wave;
-    if (lane == 0 && p0 < n) {
-      const int wd = p0 >> 5;
-      bw[wd] = (uint32_t)ob;
-      cw[wd] = (uint32_t)(onesb + opre);
-      if (wd + 1 < W) {
-        bw[wd + 1] = (uint32_t)(ob >> 32);
-        cw[wd + 1] = (uint32_t)(onesb + opre + __popc((uint32_t)ob));
+    const int ztot = __shfl(zi, 63), otot = __shfl(oi, 63);
+    const int zex = zi - zc[lane], oex = oi - oc[lane];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int zpre = __shfl(zex, j * kPrepWaves + wave), opre = __shfl(oex, j * kPrepWaves + wave);
+      if (valid[j]) aout[one[j] ? orun + opre + __popcll(ob[j] & lt) : zrun + zpre + __popcll(zb[j] & lt)] = x[j];
+      const int p0 = r0 + 1024 * j + 64 * wave;
+      if (lane == 0 && p0 < n) {
+        const int wd = p0 >> 5;
+        bw[wd] = (uint32_t)ob[j];
+        cw[wd] = (uint32_t)(onesb + opre);
+        if (wd + 1 < W) {
+          bw[wd + 1] = (uint32_t)(ob[j] >> 32);
+          cw[wd + 1] = (uint32_t)(onesb + opre + __popc((uint32_t)ob[j]));
+        }
       }
     }
     zrun += ztot;
     orun += otot;
     onesb += otot;
-    x = xn;
   }
   if (tid == 0) {
     bw[W] = 0u;
@@ -259,7 +289,7 @@ __global__ __launch_bounds__(kPrepThreads) void topk_prepare_kernel(const float*
   int32_t* rk = rank + (size_t)seg * T;
   int32_t* ps = w.ps;
 
-  for (int i = tid; i < kPrepWaves * 256; i += kPrepThreads) (&sm.cnt[0][0])[i] = 0;
+  for (int i = tid; i < kSortJ * kPrepWaves * 256; i += kPrepThreads) (&sm.cnt[0][0][0])[i] = 0;
   // Keys and positions; no fma contraction, to match fl(r - fl(t * lg)).
   for (int t = tid; t < T; t += kPrepThreads) {
     w.ka[t] = desc_key(static_priority(r[t], (float)t, lg));
@@ -284,12 +314,21 @@ __global__ __launch_bounds__(kPrepThreads) void topk_prepare_kernel(const float*
   if (n <= 0) return;
 
   // A_i = rank_{s+i} and its prefix maxima (the boundary token before saturation),
-  // one coalesced round of 1024 positions at a time.
+  // one coalesced round of 1024 positions at a time; also the number of A values
+  // with each bit set, which every wavelet level needs.
+  if (tid < 32) sm.bitcnt[tid] = 0;
+  int bits[32];
+#pragma unroll
+  for (int k = 0; k < 32; ++k) bits[k] = 0;
   int run = INT32_MIN;
   for (int r0 = 0; r0 < n; r0 += kPrepThreads) {
     const int i = r0 + tid;
     const int av = i < n ? rk[s + i] : INT32_MIN;
-    if (i < n) w.ka[i] = (uint32_t)av;
+    if (i < n) {
+      w.ka[i] = (uint32_t)av;
+#pragma unroll
+      for (int k = 0; k < 32; ++k) bits[k] += (av >> k) & 1;
+    }
     int total;
     const int ex = block_scan<true>(av, sm.sh, total);
     if (i < n) w.pmax[i] = max(run, max(ex, av));
@@ -297,11 +336,20 @@ __global__ __launch_bounds__(kPrepThreads) void topk_prepare_kernel(const float*
   }
   __syncthreads();
 
+#pragma unroll
+  for (int k = 0; k < 32; ++k) {
+    int c = bits[k];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off);
+    if ((tid & 63) == 0 && k < L) atomicAdd(&sm.bitcnt[k], c);
+  }
+  __syncthreads();
+
   // Wavelet matrix: level l splits on bit L-1-l of the current array (stable).
   const int W = (n + 31) / 32;
   uint32_t *ain = w.ka, *aout = w.kb;
   for (int l = 0; l < L; ++l) {
-    const uint32_t z = wavelet_level(ain, aout, n, L - 1 - l, w.bits + (size_t)l * (W + 1),
+    const uint32_t z = wavelet_level(ain, aout, n, L - 1 - l, sm.bitcnt[L - 1 - l], w.bits + (size_t)l * (W + 1),
                                      w.cnt + (size_t)l * (W + 1), sm);
     if (tid == 0) w.zeros[l] = z;
     uint32_t* t0 = ain;
