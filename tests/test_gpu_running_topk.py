@@ -116,3 +116,20 @@ def test_paper_budget_at_benchmark_size():
             assert np.array_equal(np.sort(got["rank"][b, h]), np.arange(T))
             c = got["cutoff"][b, h]
             assert np.all(np.diff(c[s + w + k - 1:]) <= 0) and np.all(c[:s + w + k - 1] == T)
+
+
+def test_long_context_t131072():
+    """T = 131072 (the long-context workload's length), paper budget, decay on: ranks,
+    cutoffs and eviction queries of two heads in full, labels and boundaries sampled."""
+    H, T, s, w, k = 4, 131072, 4, 256, 2016
+    rng = np.random.default_rng(21)
+    scores = rng.standard_normal((1, H, T)).astype(np.float32)
+    log_gamma = np.log(np.linspace(0.999, 0.999999, H)).astype(np.float32)
+    got = _run(scores, log_gamma, s, w, k)
+    qs = sorted(set(rng.integers(0, T, 48).tolist()) | {0, s + w + k - 1, T - 1})
+    for h in (0, 3):
+        e = _expected(scores[:, h:h + 1], log_gamma[h:h + 1], s, w, k, queries=qs)
+        for n in ("rank", "cutoff", "evict"):
+            np.testing.assert_array_equal(got[n][0, h], e[n][0, 0], err_msg=n)
+        np.testing.assert_array_equal(got["label"][0, h, qs], e["label"][0, 0, qs])
+        np.testing.assert_array_equal(got["boundary"][0, h, qs], e["boundary"][0, 0, qs])

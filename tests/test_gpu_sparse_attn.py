@@ -230,3 +230,34 @@ def test_large_logits_take_the_exact_path():
     for qh in range(4):
         _check_rows(o[0, qh], lse[0, qh], wl.q_bits[0, qh], k_bits[0, 0], v_bits[0, 0],
                     wl.scale, M, rows, None, "qh%d" % qh)
+
+
+def test_long_context_t131072():
+    """The long-context workload (B=1, 32/8 heads, D=128, T=131072, clustered keys) under
+    the paper's budget: sampled query rows of two KV-head groups, every head."""
+    s, w, k = 4, 256, 2016
+    wl = workload.make("long_t128k")
+    T, Hq, Hkv = wl.T, wl.Hq, wl.Hkv
+    v_bits = workload.make_values(wl)
+    scores = workload.make_scores(wl)
+    evict, _, cut_g = _gpu_ranking(scores, s, w, k)
+    o, lse = kv.kvpop_sparse_attn_fwd(_dev(wl.q_bits), _dev(wl.k_bits), _dev(v_bits), evict, wl.scale)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(22)
+    rows = np.array(sorted(set(rng.integers(0, T, 16).tolist()) | {0, 4095, 4096, 65535, 65536, T - 1}))
+    G = Hq // Hkv
+    rows_dev = torch.from_numpy(rows).to("cuda")
+    for h in (0, 6):
+        rank = oracle.ranks_from_priority(oracle.static_priority_f32(scores[0, h], 0.0))
+        tau = oracle.running_cutoff_fenwick(rank, s, w, k)
+        np.testing.assert_array_equal(cut_g[0, h], tau)
+        M = oracle.running_topk_mask_rows(rank, tau, s, w, rows)
+        for g in range(G):
+            qh = h * G + g
+            full = np.zeros((T, wl.D))
+            full[rows] = _bf16_to_f64(o[0, qh, rows_dev])
+            lse_full = np.zeros(T)
+            lse_full[rows] = lse[0, qh, rows_dev].cpu().numpy()
+            _check_rows(full, lse_full, wl.q_bits[0, qh], wl.k_bits[0, h], v_bits[0, h], wl.scale, M, rows, wl.bias,
+                        "qh%d" % qh)
+    assert torch.isfinite(lse).all()
