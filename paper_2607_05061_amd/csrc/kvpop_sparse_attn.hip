@@ -222,7 +222,7 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
   using SM = Smem<D, HAS_BIAS>;
   constexpr int KS = SM::KS, DB = SM::DB;
   static_assert(KS == 4 || KS == 8, "head dim 64 or 128");
-  constexpr int RUN = EXACT ? 1 : kRun;  // tiles per workgroup
+  constexpr int RUN = kRun;  // tiles per workgroup
   __shared__ __attribute__((aligned(16))) SM sm;
 
   const int tid = threadIdx.x;
@@ -490,16 +490,30 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
   int cntA = 0, cntP = 0;  // list sizes (without padding)
   bool lists_ok = false;   // the lists hold every key of the previous tile
 
+  // The exact variant leaves at once when the fast one flagged no tile of the run.
+  if (EXACT) {
+    int flagged = 0;
+    for (int tile = run * RUN; tile < tile_end; ++tile) {
+      const int r = tile * a.qt + qcol;
+      flagged |= r < T ? __builtin_isnan(a.lse[((size_t)b * a.Hq + qh) * T + r]) : 0;
+    }
+    if (!__syncthreads_or(flagged)) return;
+  }
+
   for (int tile = run * RUN; tile < tile_end; ++tile) {
     const int pq1 = q1;
     q0 = tile * a.qt;
     q1 = min(q0 + a.qt, T) - 1;
     qrow = q0 + qcol;
 
-    // The exact variant only redoes tiles the fast variant flagged (NaN in lse).
+    // The exact variant only redoes tiles the fast variant flagged (NaN in lse); a
+    // skipped tile leaves no lists for the next one.
     if (EXACT) {
       const int flagged = qrow < T ? __builtin_isnan(a.lse[((size_t)b * a.Hq + qh) * T + qrow]) : 0;
-      if (!__syncthreads_or(flagged)) return;
+      if (!__syncthreads_or(flagged)) {
+        lists_ok = false;
+        continue;
+      }
     }
 
     // Q column in registers as the B operand of S^T = K Q^T: k-step s uses the
@@ -706,14 +720,13 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
   }
 }
 
-// The fast variant (runs of kRun tiles per workgroup), then the exact one (one tile
-// per workgroup), which exits at once on tiles the fast one did not flag.
+// The fast variant, then the exact one, which skips at once every tile the fast one
+// did not flag. Both give each workgroup a run of kRun tiles.
 template <int D, int HPW, bool HB>
 int launch_d(const SparseLaunch& L) {
   const unsigned groups = (unsigned)(L.B * L.Hkv * L.nch);
-  const unsigned grid_fast = (unsigned)((L.ntiles + kRun - 1) / kRun) * groups;
-  const unsigned grid = (unsigned)L.ntiles * groups;
-  hipLaunchKernelGGL((sparse_attn_fwd_kernel<D, HPW, HB, false>), dim3(grid_fast), dim3(kThreads), 0,
+  const unsigned grid = (unsigned)((L.ntiles + kRun - 1) / kRun) * groups;
+  hipLaunchKernelGGL((sparse_attn_fwd_kernel<D, HPW, HB, false>), dim3(grid), dim3(kThreads), 0,
                      (hipStream_t)L.stream, L);
   int e = (int)hipGetLastError();
   if (e) return e;
