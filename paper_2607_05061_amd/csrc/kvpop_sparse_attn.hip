@@ -61,7 +61,7 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kRsrcWord3 = 0x00020000;  // raw (untyped) buffer access
 constexpr float kRescale = 8.0f;        // lazy-maximum slack of the exact variant, log2 units
-constexpr float kOverflow = 64.0f;      // fast variant: largest term above the reference, log2 units
+constexpr float kOverflowSum = 0x1p64f; // fast variant: largest block sum of terms relative to the reference
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kScan = 1024;             // positions per scan step (2 per thread)
@@ -370,16 +370,19 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
 
   // Softmax numerators of a block: reference maximum, exponentials, row sum and
   // bf16 packing into the B operand of the PV product.
-  auto softmax = [&](f32x16& x, bf16x8 (&pk)[2]) __attribute__((always_inline)) {
+  auto block_max = [&](const f32x16& x) __attribute__((always_inline)) {
     float mx = x[0];
 #pragma unroll
     for (int r = 1; r < 16; ++r) mx = fmaxf(mx, x[r]);
     float m0, m1;
     pair_values(mx, m0, m1);
     mx = fmaxf(m0, m1);
-    if (!HAS_BIAS) mx *= a.c;  // log2 units
+    return HAS_BIAS ? mx : mx * a.c;  // log2 units
+  };
+  auto softmax = [&](f32x16& x, bf16x8 (&pk)[2]) __attribute__((always_inline)) {
     if (EXACT) {
       // Online maximum with lazy rescaling of the accumulators.
+      const float mx = block_max(x);
       if (mx > m + kRescale) {
         const float f = __builtin_amdgcn_exp2f(m - mx);
 #pragma unroll
@@ -387,19 +390,25 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
         l *= f;
         m = mx;
       }
-    } else {
-      // Fixed reference: the first finite block maximum. Later terms up to 2^64 are
-      // exact in fp32 and bf16; beyond that the column is flagged.
+    } else if (__builtin_amdgcn_ballot_w64(m == -__builtin_inff()) != 0) {
+      // Fixed reference: the first finite block maximum, so the maximum is taken
+      // only until every column of the wave has one.
+      const float mx = block_max(x);
       if (m == -__builtin_inff()) m = mx;
-      ovf = ovf || mx > m + kOverflow;
     }
     const float mu = m == -__builtin_inff() ? 0.f : m;
-    float p[16];
+    float p[16], ts[2] = {0.f, 0.f};
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       p[r] = HAS_BIAS ? __builtin_amdgcn_exp2f(x[r] - mu) : __builtin_amdgcn_exp2f(__builtin_fmaf(x[r], a.c, -mu));
-      l += p[r];
+      ts[r & 1] += p[r];
     }
+    const float t = ts[0] + ts[1];
+    l += t;
+    // Fast variant: terms up to 2^64 above the reference are exact in fp32 and bf16.
+    // A block sum beyond that (or inf) means some term may exceed it, and the column
+    // is flagged.
+    if (!EXACT) ovf = ovf || !(t <= kOverflowSum);
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) {
       f32x8 v8;
