@@ -188,6 +188,19 @@ __device__ __forceinline__ void kfrag_wait(KFrag<8>& f) {
                  "+v"(f.r[7]));
 }
 
+// Wait for the K fragments issued just before a block's V reads (8 of them for a
+// 32-key block at head dim 64, 16 at 128): LDS reads complete in order, so with at
+// most 15 (the counter's limit) or 8 reads outstanding the K reads have landed.
+__device__ __forceinline__ void kfrag_wait_before_v(KFrag<8>& f) {
+  asm volatile("s_waitcnt lgkmcnt(15)"
+               : "+v"(f.r[0]), "+v"(f.r[1]), "+v"(f.r[2]), "+v"(f.r[3]), "+v"(f.r[4]), "+v"(f.r[5]), "+v"(f.r[6]),
+                 "+v"(f.r[7]));
+}
+
+__device__ __forceinline__ void kfrag_wait_before_v(KFrag<4>& f) {
+  asm volatile("s_waitcnt lgkmcnt(8)" : "+v"(f.r[0]), "+v"(f.r[1]), "+v"(f.r[2]), "+v"(f.r[3]));
+}
+
 __device__ __forceinline__ void kfrag_issue(KFrag<4>& f, uint32_t a) {
   asm volatile(
       "ds_read_b128 %0, %4 offset:0\n ds_read_b128 %1, %4 offset:1024\n"
@@ -671,9 +684,12 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
         }
         wait_block(min(nbt, 3) - 1);
         block_barrier();
-        f32x16 sc;
-        qk(0, sc);
-        for (int i = 0; i < nbt; ++i) {
+        // One iteration: block i's scores arrive in sc, block i + 1's leave in sn.
+        // The K reads of block i + 1 go out before the V reads of block i, so the
+        // QK^T product starts once they land. Its MFMAs are interleaved with block
+        // i's exponentials, and the PV MFMAs (k-half major, so no two in a row
+        // share an accumulator) with the packing and the row sums.
+        auto iter = [&](int i, f32x16& sc, f32x16& sn) __attribute__((always_inline)) {
           if (i + 1 < nbt) {
             wait_block(i + 2 < nbt ? 1 : 0);
             block_barrier();  // block i + 1 landed everywhere; block i - 1's buffer is free
@@ -683,22 +699,74 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
             issue(lp, blk, (i + 3) & 3);
           }
           // Block i + 1's K fragments (on the last iteration a stale buffer; the
-          // scores are unused) and block i's V fragments, read without the compiler's
-          // waits for the copies in flight.
+          // scores are unused) and block i's V fragments, read without the
+          // compiler's waits for the copies in flight.
           KFrag<KS> kf;
           kfrag_issue(kf, lds_addr(sm.ktile[(i + 1) & 3] + lane * 8));
           VFrag<DB> vf;
           vfrag_issue(vf, lds_addr(sm.vtile[i & 3] + lane * 4));
           source(i, lp, msk, n, blk);
           prep(sc, lp, sm.lenP, msk, n, blk, i & 3);
-          kfrag_wait(kf);
-          f32x16 sn;
-          qk_regs(kf, sn);
+          if (__builtin_amdgcn_ballot_w64(m == -__builtin_inff()) != 0) {
+            // Fixed reference: the first finite block maximum, taken only until
+            // every column of the wave has one.
+            const float mx = block_max(sc);
+            if (m == -__builtin_inff()) m = mx;
+          }
+          const float mu = m == -__builtin_inff() ? 0.f : m;
+          kfrag_wait_before_v(kf);
+          __builtin_amdgcn_sched_barrier(0);
+          constexpr int EPK = 16 / KS;  // exponentials per QK^T k-step
+          float p[16];
+          sn = f32x16{};
+#pragma unroll
+          for (int st = 0; st < KS; ++st) {
+            sn = mfma32(kf.r[st], qf[st], sn);
+#pragma unroll
+            for (int e = 0; e < EPK; ++e) {
+              const int r = st * EPK + e;
+              p[r] = HAS_BIAS ? __builtin_amdgcn_exp2f(sc[r] - mu)
+                              : __builtin_amdgcn_exp2f(__builtin_fmaf(sc[r], a.c, -mu));
+            }
+            __builtin_amdgcn_sched_barrier(0);
+          }
           bf16x8 pk[2];
-          softmax(sc, pk);
+#pragma unroll
+          for (int k2 = 0; k2 < 2; ++k2) {
+            f32x8 v8;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) v8[j] = p[8 * k2 + j];
+            pk[k2] = __builtin_convertvector(v8, bf16x8);
+          }
           vfrag_wait(vf);
-          pv(vf, pk);
-          sc = sn;
+          __builtin_amdgcn_sched_barrier(0);
+          float ts[2] = {0.f, 0.f};
+#pragma unroll
+          for (int k2 = 0; k2 < 2; ++k2) {
+#pragma unroll
+            for (int d = 0; d < DB; ++d) {
+              const i16x4 lo = vf.r[4 * d + 2 * k2], up = vf.r[4 * d + 2 * k2 + 1];
+              const i16x8 w8 = {lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
+              o[d] = mfma32(__builtin_bit_cast(bf16x8, w8), pk[k2], o[d]);
+#pragma unroll
+              for (int e = 0; e < 8 / DB; ++e) {
+                const int r = 8 * k2 + (8 / DB) * d + e;
+                ts[r & 1] += p[r];
+              }
+              __builtin_amdgcn_sched_barrier(0);
+            }
+          }
+          const float t = ts[0] + ts[1];
+          l += t;
+          // Terms up to 2^64 above the reference are exact in fp32 and bf16. A block
+          // sum beyond that (or inf) means some term may exceed it: flag the column.
+          ovf = ovf || !(t <= kOverflowSum);
+        };
+        f32x16 sa, sb;
+        qk(0, sa);
+        for (int i = 0; i < nbt; i += 2) {
+          iter(i, sa, sb);
+          if (i + 1 < nbt) iter(i + 1, sb, sa);
         }
         __syncthreads();
       }
