@@ -27,7 +27,18 @@ sys.path.insert(0, ROOT)
 
 METRIC = "key-query pairs/sec and MFMA util (% bf16 peak), Qwen3-8B-shaped layer at T=32k"
 PEAK_BF16_TFLOPS = 2516.6  # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 flop/clk/CU
-KERNEL_SRC = os.path.join(ROOT, "paper_2607_05061_amd", "csrc", "kvpop_kernels.hip")
+CSRC = os.path.join(ROOT, "paper_2607_05061_amd", "csrc")
+# The source file of each kernel whose HBM traffic is recorded (the fast and exact
+# variants of the sparse forward are told apart by their last template argument).
+KERNEL_SOURCES = {
+    "row_lse_kernel": "kvpop_kernels.hip",
+    "future_mass_kernel": "kvpop_kernels.hip",
+    "sparse_attn_fwd_kernel": "kvpop_sparse_attn.hip",
+    "sparse_attn_fwd_kernel_exact": "kvpop_sparse_attn.hip",
+    "topk_prepare_kernel": "kvpop_topk.hip",
+    "topk_query_kernel": "kvpop_topk.hip",
+    "topk_evict_kernel": "kvpop_topk.hip",
+}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 TOPK_BUDGET = (4, 256, 2016)  # sinks s, protected window w, top-k k: the paper's fixed budget B = s + w + k = 2276
 
@@ -45,23 +56,33 @@ def band_pairs(T: int, window: int, horizon: int) -> int:
     return n * T - (window + hi) * n // 2
 
 
-def kernel_source_hash() -> str:
-    with open(KERNEL_SRC, "rb") as f:
+def kernel_source_hash(kernel: str) -> str:
+    with open(os.path.join(CSRC, KERNEL_SOURCES[kernel]), "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()
+
+
+def kernel_key(name: str):
+    """The KERNEL_SOURCES key of a profiled kernel name, or None."""
+    if "sparse_attn_fwd_kernel" in name:
+        args = name.split("sparse_attn_fwd_kernel", 1)[1]
+        args = args[:args.index(">")] if ">" in args else args
+        return "sparse_attn_fwd_kernel_exact" if args.rstrip().endswith("true") else "sparse_attn_fwd_kernel"
+    for k in KERNEL_SOURCES:
+        if k in name:
+            return k
+    return None
 
 
 def traffic_for(kernel: str, workload: str):
     """HBM bytes per launch from committed rocprofv3 counter summaries, or None when
-    absent or taken on a different kernel source."""
+    absent or taken on a different source of that kernel."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("kernel_source_sha256") != kernel_source_hash() or t.get("workload") != workload:
-        return None
     k = t.get("kernels", {}).get(kernel)
-    if not k:
+    if t.get("workload") != workload or not k or k.get("source_sha256") != kernel_source_hash(kernel):
         return None
     return k.get("hbm_bytes_per_launch")
 
@@ -127,9 +148,11 @@ def traffic_summary(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, worklo
                 if r["Counter_Name"] != counter:
                     continue
                 name = r["Kernel_Name"]
-                for key in ("row_lse_kernel", "future_mass_kernel", "copy", "elementwise"):
-                    if key in name:
-                        vals.setdefault(key, []).append(float(r["Counter_Value"]))
+                key = kernel_key(name)
+                if key is None:
+                    key = next((c for c in ("copy", "elementwise") if c in name), None)
+                if key is not None:
+                    vals.setdefault(key, []).append(float(r["Counter_Value"]))
         return vals
 
     def copy_factor(d, counter):
@@ -143,13 +166,14 @@ def traffic_summary(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, worklo
     fetch = per_kernel(fetch_dir, "FETCH_SIZE")
     write = per_kernel(write_dir, "WRITE_SIZE")
     kernels = {}
-    for k in ("row_lse_kernel", "future_mass_kernel"):
+    for k in KERNEL_SOURCES:
         if k in fetch and k in write:
             fb = sum(fetch[k]) / len(fetch[k]) * 1024.0 * ff
             wb = sum(write[k]) / len(write[k]) * 1024.0 * wf
             kernels[k] = {"fetch_bytes_per_launch": fb, "write_bytes_per_launch": wb,
-                          "hbm_bytes_per_launch": fb + wb, "launches": len(fetch[k])}
-    res = {"workload": workload, "kernel_source_sha256": kernel_source_hash(),
+                          "hbm_bytes_per_launch": fb + wb, "launches": len(fetch[k]),
+                          "source": KERNEL_SOURCES[k], "source_sha256": kernel_source_hash(k)}
+    res = {"workload": workload,
            "copy_calibration": {"bytes": COPY_BYTES, "fetch_kib_read": fk, "write_kib_read": wk,
                                 "fetch_factor": ff, "write_factor": wf},
            "kernels": kernels}

@@ -344,12 +344,6 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
       sacc = mfma32(*reinterpret_cast<const bf16x8*>(kt + s * kPlane + lane * 8), qf[s], sacc);
   };
 
-  // The same product from fragments read by kfrag_issue.
-  auto qk_regs = [&](const KFrag<KS>& f, f32x16& sacc) __attribute__((always_inline)) {
-    sacc = f32x16{};
-#pragma unroll
-    for (int s = 0; s < KS; ++s) sacc = mfma32(f.r[s], qf[s], sacc);
-  };
 
   // Key bias and masking of block `blk` of a list (entries lpos/llen, n of them):
   // with a bias, logits in log2 units in place; without one the raw scores stay
@@ -381,8 +375,7 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
     }
   };
 
-  // Softmax numerators of a block: reference maximum, exponentials, row sum and
-  // bf16 packing into the B operand of the PV product.
+  // Largest logit of a block for this lane's column (both lane halves), log2 units.
   auto block_max = [&](const f32x16& x) __attribute__((always_inline)) {
     float mx = x[0];
 #pragma unroll
@@ -392,36 +385,26 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
     mx = fmaxf(m0, m1);
     return HAS_BIAS ? mx : mx * a.c;  // log2 units
   };
-  auto softmax = [&](f32x16& x, bf16x8 (&pk)[2]) __attribute__((always_inline)) {
-    if (EXACT) {
-      // Online maximum with lazy rescaling of the accumulators.
-      const float mx = block_max(x);
-      if (mx > m + kRescale) {
-        const float f = __builtin_amdgcn_exp2f(m - mx);
+  // The exact variant's softmax numerators of a block: online maximum with lazy
+  // rescaling of the accumulators, exponentials, row sum and bf16 packing into the B
+  // operand of the PV product. (The fast variant's, against a fixed reference, are
+  // interleaved with the next block's QK^T product in its block loop.)
+  auto softmax_exact = [&](f32x16& x, bf16x8 (&pk)[2]) __attribute__((always_inline)) {
+    const float mx = block_max(x);
+    if (mx > m + kRescale) {
+      const float f = __builtin_amdgcn_exp2f(m - mx);
 #pragma unroll
-        for (int d = 0; d < DB; ++d) o[d] *= f;
-        l *= f;
-        m = mx;
-      }
-    } else if (__builtin_amdgcn_ballot_w64(m == -__builtin_inff()) != 0) {
-      // Fixed reference: the first finite block maximum, so the maximum is taken
-      // only until every column of the wave has one.
-      const float mx = block_max(x);
-      if (m == -__builtin_inff()) m = mx;
+      for (int d = 0; d < DB; ++d) o[d] *= f;
+      l *= f;
+      m = mx;
     }
     const float mu = m == -__builtin_inff() ? 0.f : m;
-    float p[16], ts[2] = {0.f, 0.f};
+    float p[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       p[r] = HAS_BIAS ? __builtin_amdgcn_exp2f(x[r] - mu) : __builtin_amdgcn_exp2f(__builtin_fmaf(x[r], a.c, -mu));
-      ts[r & 1] += p[r];
+      l += p[r];
     }
-    const float t = ts[0] + ts[1];
-    l += t;
-    // Fast variant: terms up to 2^64 above the reference are exact in fp32 and bf16.
-    // A block sum beyond that (or inf) means some term may exceed it, and the column
-    // is flagged.
-    if (!EXACT) ovf = ovf || !(t <= kOverflowSum);
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) {
       f32x8 v8;
@@ -665,7 +648,7 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
           qk(i & 3, x);
           prep(x, lp, sm.lenP, msk, n, blk, i & 3);
           bf16x8 pk[2];
-          softmax(x, pk);
+          softmax_exact(x, pk);
           VFrag<DB> vf;
           vfrag_issue(vf, lds_addr(sm.vtile[i & 3] + lane * 4));
           vfrag_wait(vf);
