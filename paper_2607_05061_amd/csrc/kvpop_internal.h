@@ -55,6 +55,7 @@ struct SparseLaunch {
   void* stream;
   // plan
   int32_t G, hpw, wq, qt, hc, nch, ntiles;
+  int32_t run;            // query tiles per workgroup
   float c;                // scale * log2(e)
 };
 void sparse_attn_plan(SparseLaunch& L);

@@ -71,7 +71,8 @@ constexpr int kPlane = 512;             // bf16 elements per 1 KB plane
 constexpr int kBufs = 4;                // K/V block buffers (see the block loop)
 constexpr int kChunk = 4096;            // lifetimes staged into LDS per chunk (16 KB)
 constexpr int kEvBufs = 2;              // chunk buffers: the next chunk loads during the scan
-constexpr int kRun = 8;                 // query tiles per workgroup (fast variant)
+constexpr int kRunMax = 8;              // most query tiles per workgroup
+constexpr int kRunGrid = 1024;          // workgroups wanted before runs grow
 
 __device__ __forceinline__ constexpr int acc_row(int r, int hi) { return 8 * (r >> 2) + 4 * hi + (r & 3); }
 
@@ -235,7 +236,7 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
   using SM = Smem<D, HAS_BIAS>;
   constexpr int KS = SM::KS, DB = SM::DB;
   static_assert(KS == 4 || KS == 8, "head dim 64 or 128");
-  constexpr int RUN = kRun;  // tiles per workgroup
+  const int RUN = a.run;  // tiles per workgroup
   __shared__ __attribute__((aligned(16))) SM sm;
 
   const int tid = threadIdx.x;
@@ -781,11 +782,11 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
 }
 
 // The fast variant, then the exact one, which skips at once every tile the fast one
-// did not flag. Both give each workgroup a run of kRun tiles.
+// did not flag. Both give each workgroup a run of L.run tiles.
 template <int D, int HPW, bool HB>
 int launch_d(const SparseLaunch& L) {
   const unsigned groups = (unsigned)(L.B * L.Hkv * L.nch);
-  const unsigned grid = (unsigned)((L.ntiles + kRun - 1) / kRun) * groups;
+  const unsigned grid = (unsigned)((L.ntiles + L.run - 1) / L.run) * groups;
   hipLaunchKernelGGL((sparse_attn_fwd_kernel<D, HPW, HB, false>), dim3(grid), dim3(kThreads), 0,
                      (hipStream_t)L.stream, L);
   int e = (int)hipGetLastError();
@@ -815,6 +816,11 @@ void sparse_attn_plan(SparseLaunch& L) {
   L.hc = L.hpw * nhp;
   L.nch = L.G / L.hc;
   L.ntiles = (L.T + L.qt - 1) / L.qt;
+  // Runs of consecutive tiles share their key lists, but each run is one workgroup:
+  // shorten them until the launch has about kRunGrid workgroups (4 per CU).
+  const long long tiles = (long long)L.ntiles * L.B * L.Hkv * L.nch;
+  const long long r = tiles / kRunGrid;
+  L.run = r < 1 ? 1 : (r > kRunMax ? kRunMax : (int)r);
   L.c = L.scale * kLog2e;
 }
 

@@ -102,6 +102,17 @@ def test_matches_oracle(case):
     _run_case(*case, seed=sum(case))
 
 
+def test_runs_of_several_tiles_with_ragged_ends():
+    """B=4, 32 query / 8 KV heads, T=8092: 127 query tiles of 64 per group and 32
+    groups, so each workgroup takes a run of 3 consecutive tiles (the last run holds
+    one) and rebuilds its key lists incrementally from tile to tile; the last tile
+    has 28 queries. Rows of the first run, around a run boundary and of the last
+    tile, every head of every group."""
+    T = 8092
+    rows = np.r_[0:3, 60:70, 127:130, 189:195, 62 * 64 - 3:63 * 64 + 3, 126 * 64 - 2:T]
+    _run_case(4, 32, 8, T, 128, 4, 256, 512, seed=21, rows=rows)
+
+
 def test_sink_bias():
     """The +3 logit sink of the synthetic workloads as a key bias."""
     _run_case(1, 8, 2, 400, 128, 4, 32, 50, seed=7, sink=True)
