@@ -476,6 +476,11 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
       totA += ca;
       totP += cp;
     }
+    // Every lane read the same counts: keep the sums in scalar registers.
+    befA = __builtin_amdgcn_readfirstlane(befA);
+    befP = __builtin_amdgcn_readfirstlane(befP);
+    totA = __builtin_amdgcn_readfirstlane(totA);
+    totP = __builtin_amdgcn_readfirstlane(totP);
     const bool fits = nA + totA <= kCapA && nP + totP <= kCapP;
     if (fits && full) {
       const int i = nA + befA + __builtin_amdgcn_mbcnt_hi((uint32_t)(bf >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bf, 0));
@@ -621,6 +626,10 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
       lds_sync();  // the lists are complete and visible to every wave
 
       // Blocks of list A (no per-element test) then of list P.
+      // The list sizes are the same in every lane (sums of counts read back from
+      // LDS); taking them from lane 0 lets the block loop branch on scalars.
+      cntA = __builtin_amdgcn_readfirstlane(cntA);
+      cntP = __builtin_amdgcn_readfirstlane(cntP);
       const int nbA = (cntA + 31) >> 5;
       const int nbt = nbA + ((cntP + 31) >> 5);
       auto source = [&](int i, const int*& lp, bool& msk, int& n, int& blk) __attribute__((always_inline)) {
