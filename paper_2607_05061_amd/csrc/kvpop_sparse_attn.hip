@@ -68,7 +68,7 @@ constexpr int kScan = 1024;             // positions per scan step (2 per thread
 constexpr int kCapA = 4096;             // list A capacity (entries)
 constexpr int kCapP = 1536;             // list P capacity (entries)
 constexpr int kPlane = 512;             // bf16 elements per 1 KB plane
-constexpr int kBufs = 4;                // K/V block buffers (see the block loop)
+constexpr int kBufs = 5;                // K/V block buffers (see the block loop)
 constexpr int kChunk = 4096;            // lifetimes staged into LDS per chunk (16 KB)
 constexpr int kEvBufs = 2;              // chunk buffers: the next chunk loads during the scan
 constexpr int kRunMax = 8;              // most query tiles per workgroup
@@ -643,24 +643,24 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
       int n, blk;
       if (EXACT && nbt > 0) {
         // Unpipelined: block i + 1 is gathered while block i is computed; buffer
-        // i & 3 is refilled at iteration i + 3, after two more barriers.
+        // i % kBufs is refilled at iteration i + kBufs - 1, after more barriers.
         source(0, lp, msk, n, blk);
         issue(lp, blk, 0);
         for (int i = 0; i < nbt; ++i) {
           if (i + 1 < nbt) {
             source(i + 1, lp, msk, n, blk);
-            issue(lp, blk, (i + 1) & 3);
+            issue(lp, blk, (i + 1) % kBufs);
           }
           wait_block(i + 1 < nbt ? 1 : 0);
           block_barrier();
           source(i, lp, msk, n, blk);
           f32x16 x;
-          qk(i & 3, x);
-          prep(x, lp, sm.lenP, msk, n, blk, i & 3);
+          qk(i % kBufs, x);
+          prep(x, lp, sm.lenP, msk, n, blk, i % kBufs);
           bf16x8 pk[2];
           softmax_exact(x, pk);
           VFrag<DB> vf;
-          vfrag_issue(vf, lds_addr(sm.vtile[i & 3] + lane * 4));
+          vfrag_issue(vf, lds_addr(sm.vtile[i % kBufs] + lane * 4));
           vfrag_wait(vf);
           pv(vf, pk);
         }
@@ -668,9 +668,12 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
       } else if (nbt > 0) {
         // Software pipeline over the blocks. Iteration i computes the scores of
         // block i + 1 (MFMA) while it turns block i's scores into probabilities
-        // (VALU), then multiplies block i's probabilities with its values. Blocks
-        // i + 2 and i + 3 are being gathered meanwhile; with 4 buffers, the one
-        // refilled at iteration i held block i - 1, finished at iteration i - 1.
+        // (VALU), then multiplies block i's probabilities with its values. The
+        // workgroup meets at a barrier on even iterations only: barrier i certifies
+        // blocks i + 1 and i + 2 (copied since barrier i - 2), after which blocks
+        // i + 3 and i + 4 are copied into the buffers of blocks i - 2 and i - 1,
+        // which every wave finished with in iteration i - 1. Blocks i .. i + 4 are
+        // live, one buffer each.
         for (int j = 0; j < 3 && j < nbt; ++j) {
           source(j, lp, msk, n, blk);
           issue(lp, blk, j);
@@ -682,24 +685,27 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
         // QK^T product starts once they land. Its MFMAs are interleaved with block
         // i's exponentials, and the PV MFMAs (k-half major, so no two in a row
         // share an accumulator) with the packing and the row sums.
-        auto iter = [&](int i, f32x16& sc, f32x16& sn) __attribute__((always_inline)) {
-          if (i + 1 < nbt) {
-            wait_block(i + 2 < nbt ? 1 : 0);
-            block_barrier();  // block i + 1 landed everywhere; block i - 1's buffer is free
-          }
-          if (i + 3 < nbt) {
-            source(i + 3, lp, msk, n, blk);
-            issue(lp, blk, (i + 3) & 3);
+        auto iter = [&](int i, f32x16& sc, f32x16& sn, bool even) __attribute__((always_inline)) {
+          if (even && i + 1 < nbt) {
+            wait_vmcnt<0>();  // this wave's copies of blocks i + 1 and i + 2
+            block_barrier();
+#pragma unroll
+            for (int j = 3; j <= 4; ++j) {
+              if (i + j < nbt) {
+                source(i + j, lp, msk, n, blk);
+                issue(lp, blk, (i + j) % kBufs);
+              }
+            }
           }
           // Block i + 1's K fragments (on the last iteration a stale buffer; the
           // scores are unused) and block i's V fragments, read without the
           // compiler's waits for the copies in flight.
           KFrag<KS> kf;
-          kfrag_issue(kf, lds_addr(sm.ktile[(i + 1) & 3] + lane * 8));
+          kfrag_issue(kf, lds_addr(sm.ktile[(i + 1) % kBufs] + lane * 8));
           VFrag<DB> vf;
-          vfrag_issue(vf, lds_addr(sm.vtile[i & 3] + lane * 4));
+          vfrag_issue(vf, lds_addr(sm.vtile[i % kBufs] + lane * 4));
           source(i, lp, msk, n, blk);
-          prep(sc, lp, sm.lenP, msk, n, blk, i & 3);
+          prep(sc, lp, sm.lenP, msk, n, blk, i % kBufs);
           if (__builtin_amdgcn_ballot_w64(m == -__builtin_inff()) != 0) {
             // Fixed reference: the first finite block maximum, taken only until
             // every column of the wave has one.
@@ -758,8 +764,8 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
         f32x16 sa, sb;
         qk(0, sa);
         for (int i = 0; i < nbt; i += 2) {
-          iter(i, sa, sb);
-          if (i + 1 < nbt) iter(i + 1, sb, sa);
+          iter(i, sa, sb, true);
+          if (i + 1 < nbt) iter(i + 1, sb, sa, false);
         }
         __syncthreads();
       }
