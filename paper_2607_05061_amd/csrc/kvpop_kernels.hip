@@ -268,8 +268,9 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
   // issue order (scheduling barriers keep the compiler from regrouping it). Tile
   // u's unit runs the NQ MFMA chains of this wave's query subtiles interleaved
   // k-step by k-step, so each A fragment read from LDS feeds NQ MFMAs; the fragment
-  // register is then refilled with tile u + 1's operand (used a whole unit later),
-  // and the exp/accumulate work of tile u - 1 fills the VALU slots in between.
+  // register is then refilled with tile u + 1's operand (used a whole unit later).
+  // Each MFMA is followed by the exp/accumulate work of one subtile of tile u - 1,
+  // so the wave's VALU work issues while its MFMAs run.
   auto fast_step = [&](const uint16_t* sk, const float* sb) __attribute__((always_inline)) {
     constexpr int EPK = 16 / KS;
     float nm[NQ];
@@ -294,21 +295,22 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
       for (int n = 0; n < NQ; ++n) ts[n][0] = ts[n][1] = 0.f;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        if (u < KT) {
 #pragma unroll
-          for (int n = 0; n < NQ; ++n) acc[n] = mfma32(fr[ks], qf[n][ks], acc[n]);
-          if (u + 1 < KT) fr[ks] = TL::frag(sk + (u + 1) * TL::ELEMS, lane, ks);
-        }
-        if (u > 0) {
-#pragma unroll
-          for (int n = 0; n < NQ; ++n)
+        for (int n = 0; n < NQ; ++n) {
+          // one MFMA, then the exponentials of one subtile of the previous tile
+          if (u < KT) {
+            acc[n] = mfma32(fr[ks], qf[n][ks], acc[n]);
+            if (n == NQ - 1 && u + 1 < KT) fr[ks] = TL::frag(sk + (u + 1) * TL::ELEMS, lane, ks);
+          }
+          if (u > 0) {
 #pragma unroll
             for (int e = 0; e < EPK; ++e) {
               const int r = ks * EPK + e;
               ts[n][e & 1] += exp2_fast(__builtin_fmaf(acc_prev[n][r], c, nm[n]));
             }
+          }
+          __builtin_amdgcn_sched_barrier(0);
         }
-        __builtin_amdgcn_sched_barrier(0);
       }
       if (u > 0) {
 #pragma unroll
@@ -526,9 +528,10 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     // Head g's unit runs the NS MFMA chains of its key subtiles interleaved k-step
     // by k-step, so each A fragment read from LDS feeds NS MFMAs; right after those
     // MFMAs the fragment register is refilled with head g + 1's operand (used a
-    // whole unit later, hiding the LDS latency), and the exp/accumulate work of
-    // head g - 1, whose accumulators completed during the previous unit, fills the
-    // VALU slots in between.
+    // whole unit later, hiding the LDS latency). Each MFMA is followed by the
+    // exp/accumulate work of one key subtile of head g - 1, whose accumulators
+    // completed during the previous unit, so the VALU work issues while the MFMAs
+    // run.
     auto full_step = [&](const uint16_t* sq, const float* sl) __attribute__((always_inline)) {
       constexpr int EPK = 16 / KS;  // elements per subtile of the previous head per k-step
       bf16x8 fr[KS];
@@ -549,21 +552,22 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
         for (int n = 0; n < NS; ++n) ts[n][0] = ts[n][1] = 0.f;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-          if (g < GC) {
 #pragma unroll
-            for (int n = 0; n < NS; ++n) acc[n] = mfma32(fr[ks], kf[n][ks], acc[n]);
-            if (g + 1 < GC) fr[ks] = TL::frag(sq + (g + 1) * TL::ELEMS, lane, ks);
-          }
-          if (g > 0) {
-#pragma unroll
-            for (int n = 0; n < NS; ++n)
+          for (int n = 0; n < NS; ++n) {
+            // one MFMA, then the exponentials of one subtile of the previous head
+            if (g < GC) {
+              acc[n] = mfma32(fr[ks], kf[n][ks], acc[n]);
+              if (n == NS - 1 && g + 1 < GC) fr[ks] = TL::frag(sq + (g + 1) * TL::ELEMS, lane, ks);
+            }
+            if (g > 0) {
 #pragma unroll
               for (int e = 0; e < EPK; ++e) {
                 const int r = ks * EPK + e;
                 ts[n][e & 1] += exp2_fast(__builtin_fmaf(acc_prev[n][r], c, nl[(g - 1) & 1][r]));
               }
+            }
+            __builtin_amdgcn_sched_barrier(0);
           }
-          __builtin_amdgcn_sched_barrier(0);
         }
         if (g > 0) {
 #pragma unroll
