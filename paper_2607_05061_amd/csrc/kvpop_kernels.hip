@@ -240,9 +240,9 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
       tmax = fmaxf(tmax, v[r]);
     }
     const float mn = fmaxf(m[n], tmax);
-    float e = 0.f;
+    float e = exp2_fast(v[0] - mn);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) e += exp2_fast(v[r] - mn);
+    for (int r = 1; r < 16; ++r) e += exp2_fast(v[r] - mn);
     sum[n] = sum[n] * exp2_fast(m[n] - mn) + e;
     m[n] = mn;
   };
@@ -306,7 +306,9 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
 #pragma unroll
             for (int e = 0; e < EPK; ++e) {
               const int r = ks * EPK + e;
-              ts[n][e & 1] += exp2_fast(__builtin_fmaf(acc_prev[n][r], c, nm[n]));
+              const float x = exp2_fast(__builtin_fmaf(acc_prev[n][r], c, nm[n]));
+              // The first terms seed the partial sums (0 + x is not folded away).
+              ts[n][e & 1] = r < 2 ? x : ts[n][e & 1] + x;
             }
           }
           __builtin_amdgcn_sched_barrier(0);
@@ -563,7 +565,9 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
 #pragma unroll
               for (int e = 0; e < EPK; ++e) {
                 const int r = ks * EPK + e;
-                ts[n][e & 1] += exp2_fast(__builtin_fmaf(acc_prev[n][r], c, nl[(g - 1) & 1][r]));
+                const float x = exp2_fast(__builtin_fmaf(acc_prev[n][r], c, nl[(g - 1) & 1][r]));
+                // The first terms seed the partial sums (0 + x is not folded away).
+                ts[n][e & 1] = r < 2 ? x : ts[n][e & 1] + x;
               }
             }
             __builtin_amdgcn_sched_barrier(0);
@@ -595,7 +599,8 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
           for (int r = 0; r < 16; ++r) {
             const int d = base + 8 * (r >> 2) + (r & 3);
             const float e = exp2_fast(__builtin_fmaf(acc[r], c, nl[r]));
-            ts += (d >= window && d <= hz) ? e : 0.f;
+            const float x = (d >= window && d <= hz) ? e : 0.f;
+            ts = r == 0 ? x : ts + x;  // the first term seeds the sum
           }
           colsum[g][n] += ts;
         }

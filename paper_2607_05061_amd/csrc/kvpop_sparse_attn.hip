@@ -739,7 +739,7 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
           }
           vfrag_wait(vf);
           __builtin_amdgcn_sched_barrier(0);
-          float ts[2] = {0.f, 0.f};
+          float ts[2] = {p[0], p[1]};  // the first terms seed the partial sums
 #pragma unroll
           for (int k2 = 0; k2 < 2; ++k2) {
 #pragma unroll
@@ -750,7 +750,7 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
 #pragma unroll
               for (int e = 0; e < 8 / DB; ++e) {
                 const int r = 8 * k2 + (8 / DB) * d + e;
-                ts[r & 1] += p[r];
+                if (r >= 2) ts[r & 1] += p[r];
               }
               __builtin_amdgcn_sched_barrier(0);
             }
