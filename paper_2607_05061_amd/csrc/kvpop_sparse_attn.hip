@@ -714,6 +714,9 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
           }
           const float mu = m == -__builtin_inff() ? 0.f : m;
           kfrag_wait_before_v(kf);
+          // Raised wave priority over the MFMA section: the arbiter then favours the
+          // wave that is feeding the matrix core over its SIMD partner's prologue.
+          __builtin_amdgcn_s_setprio(1);
           __builtin_amdgcn_sched_barrier(0);
           constexpr int EPK = 16 / KS;  // exponentials per QK^T k-step
           float p[16];
@@ -760,6 +763,7 @@ sparse_attn_fwd_kernel(SparseLaunch a) {
           // Terms up to 2^64 above the reference are exact in fp32 and bf16. A block
           // sum beyond that (or inf) means some term may exceed it: flag the column.
           ovf = ovf || !(t <= kOverflowSum);
+          __builtin_amdgcn_s_setprio(0);
         };
         f32x16 sa, sb;
         qk(0, sa);
