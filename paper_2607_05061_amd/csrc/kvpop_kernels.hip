@@ -181,7 +181,7 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
   auto tile_of = [&](int idx) __attribute__((always_inline)) { return idx < ndiag ? nkt - 1 - idx : idx - ndiag; };
 
   const int voff = TL::lane_voffset(lane);
-  float stb = 0.f;
+  float stb = 0.f;  // raw bias of this thread's key row of the next step
   auto issue = [&](int s, uint16_t* sk) __attribute__((always_inline)) {
     const int idx = s * KT + w;
     if (idx < nkt) {
@@ -191,11 +191,14 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
     if (HAS_BIAS && tid < KT * 32) {
       const int idx2 = s * KT + (tid >> 5);
       const int t = idx2 < nkt ? tile_of(idx2) * 32 + (tid & 31) : T;
-      stb = t < T ? bias[t] * inv_scale : 0.f;
+      stb = t < T ? bias[t] : 0.f;
     }
   };
+  // The arithmetic on the loaded bias stays here, after the step's compute: a use
+  // of it right after the load would wait for every outstanding vector-memory
+  // operation, the K tiles of the next step included.
   auto commit = [&](float* sb) __attribute__((always_inline)) {
-    if (HAS_BIAS && tid < KT * 32) sb[tid] = stb;
+    if (HAS_BIAS && tid < KT * 32) sb[tid] = stb * inv_scale;
   };
 
   float m[NQ], sum[NQ];
@@ -286,6 +289,8 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
     for (int u = 0; u <= KT; ++u) {
       f32x16 acc[NQ];
       if (u < KT) {
+        // One start value for all NQ chains: each chain's first MFMA reads it as
+        // its C operand, so it is never copied.
         const f32x16 a0 = acc_init(sb, u);
 #pragma unroll
         for (int n = 0; n < NQ; ++n) acc[n] = a0;
