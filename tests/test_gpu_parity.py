@@ -123,6 +123,27 @@ def test_random_bias_and_masked_keys(T):
         assert rel.max() <= REL, "bias band %s: max rel err %.3e" % ((window, horizon), rel.max())
 
 
+@pytest.mark.parametrize("T,D", [(1000, 128), (2100, 64)])
+def test_logits_far_above_the_diagonal_reference(T, D):
+    """Pass 1 takes its reference maximum from the tiles on a query block's diagonal
+    and sums later tiles against it; a tile whose terms exceed 2^64 is redone
+    exactly. Here key 0 carries a bias of +60 and keys T/2 .. T/2+4 one of +45
+    (N(0,1) inputs keep the other logits within a few units), so every query block
+    that reaches those keys below its diagonal sees terms about 2^87 and 2^65 above
+    its reference and takes the redo. LSE and future mass must still match the
+    oracle, on every key (the unbiased keys' masses are about e^-60)."""
+    w = workload.make(_cfg(1, 8, 2, T, D, seed=77 + T))
+    bias = np.zeros(T, np.float32)
+    bias[0] = 60.0
+    bias[T // 2:T // 2 + 5] = 45.0
+    lse_ref = oracle.row_lse(w.q_bits, w.k_bits, w.scale, bias)
+    for window, horizon in [(0, -1), (1, 256)]:
+        out, lse = _run(w, window, horizon, bias=bias)
+        _check_lse(lse, lse_ref, "large bias")
+        ref = oracle.future_mass(w.q_bits, w.k_bits, w.scale, bias, window, horizon, lse=lse_ref)
+        _check_out(out, ref, window, "large bias band %s" % ((window, horizon),))
+
+
 def test_tiny_config():
     """T=512, one head, D=64, N(0,1) inputs, scale 1/8, full future (window 0)."""
     w = workload.make("tiny")
