@@ -71,7 +71,7 @@ constexpr int kPlane = 512;             // bf16 elements per 1 KB plane
 constexpr int kBufs = 5;                // K/V block buffers (see the block loop)
 constexpr int kChunk = 4096;            // lifetimes staged into LDS per chunk (16 KB)
 constexpr int kEvBufs = 2;              // chunk buffers: the next chunk loads during the scan
-constexpr int kRunMax = 8;              // most query tiles per workgroup
+constexpr int kRunMax = 16;             // most query tiles per workgroup
 constexpr int kRunGrid = 1024;          // workgroups wanted before runs grow
 
 __device__ __forceinline__ constexpr int acc_row(int r, int hi) { return 8 * (r >> 2) + 4 * hi + (r & 3); }
