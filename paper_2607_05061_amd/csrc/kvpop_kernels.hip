@@ -405,7 +405,8 @@ template <int D, int NS, int GC, bool HAS_BIAS, bool EPI>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2))) void
 future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const float* __restrict__ bias,
                    const float* __restrict__ lse, float* __restrict__ out, int B, int Hq, int Hkv, int T, float c,
-                   int window, int hz, float* __restrict__ scores, int agg_mean, float eps, int normalize) {
+                   int window, int hz, float* __restrict__ scores, int agg_mean, float eps, int normalize,
+                   int xgroups) {
   using TL = Tile<D>;
   constexpr int KS = TL::KS;
   constexpr int WK = NS * 32;  // keys per wave
@@ -421,8 +422,24 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, uniform per wave
   const int G = Hq / Hkv;
   const int nbh = B * Hkv;
-  const int kb = blockIdx.x / nbh;  // key block 0 (most query rows) first
-  const int bh = blockIdx.x - kb * nbh;
+  // Workgroup order. Workgroups are dealt to the 8 XCDs round-robin (XCD =
+  // blockIdx % 8). With xgroups > 0 (B * Hkv a multiple of 8), XCD x owns the
+  // (b, KV head) groups x, x + 8, ... and runs them xgroups at a time, each batch
+  // of groups heaviest key block first: more workgroups of one group then sweep
+  // the same query tiles together and share them in that XCD's L2. Otherwise the
+  // order is key block major, heaviest first, over all groups.
+  int kb, bh;
+  if (xgroups > 0) {
+    const int nkb = (T + BK - 1) / BK;
+    const int x = (int)(blockIdx.x & 7), j = (int)(blockIdx.x >> 3);
+    const int span = xgroups * nkb;
+    const int batch = j / span, r = j - batch * span;
+    kb = r / xgroups;
+    bh = x + 8 * (batch * xgroups + r - kb * xgroups);
+  } else {
+    kb = blockIdx.x / nbh;
+    bh = blockIdx.x - kb * nbh;
+  }
   const int b = bh / Hkv;
   const int h = bh - b * Hkv;
   const int j0 = kb * BK;
@@ -687,10 +704,19 @@ int launch_p2(const Launch& L) {
   const long long grid = (long long)nkb * L.B * L.Hkv;
   const float c = L.scale * kLog2e;
   const int hz = L.horizon < 0 ? L.T : L.horizon;
+  // Groups an XCD runs at a time: half of its groups when it then still has at
+  // least 4 workgroups per slot (2 per CU on its 32 CUs), so that the second half's
+  // heaviest blocks start early enough; otherwise all of them.
+  int xgroups = 0;
+  const int nbh = L.B * L.Hkv;
+  if (nbh % 8 == 0) {
+    const int ng = nbh / 8;
+    xgroups = ng % 2 == 0 && (long long)ng * nkb >= 4 * 64 ? ng / 2 : ng;
+  }
   hipLaunchKernelGGL((future_mass_kernel<D, NS, GC, HB, EPI>), dim3((unsigned)grid), dim3(256), 0,
                      (hipStream_t)L.stream, reinterpret_cast<const uint16_t*>(L.q),
                      reinterpret_cast<const uint16_t*>(L.k), L.bias, L.lse, L.out, L.B, L.Hq, L.Hkv, L.T, c, L.window,
-                     hz, L.scores, L.agg, L.eps, L.normalize);
+                     hz, L.scores, L.agg, L.eps, L.normalize, xgroups);
   return (int)hipGetLastError();
 }
 

@@ -232,6 +232,30 @@ def test_qwen3_8b_t32k_full_scale():
         _check_out(out[b, qh, cols][None], ref[None], 0, "32k b%d qh%d tail" % (b, qh))
 
 
+def test_groups_taken_in_batches_per_xcd():
+    """64 (b, KV head) groups give each XCD 8 groups; with 32 key blocks of 256 each
+    XCD then runs them 4 at a time, one batch after the other. Every key column of
+    every head must be written exactly once (the output starts as NaN), the masses
+    of each head must sum to T (each query's probabilities sum to 1), and the first
+    and last heads must match the oracle on every key."""
+    B, H, T, D = 8, 8, 8000, 64
+    w = workload.make(dict(seed=404, B=B, Hq=H, Hkv=H, T=T, D=D, scale=1.0 / math.sqrt(D), kind="rope",
+                           sink=False, bands=[(0, -1)]))
+    q, k = _dev(w.q_bits), _dev(w.k_bits)
+    out = torch.full((B, H, T), float("nan"), device="cuda")
+    lse = torch.empty((B, H, T), device="cuda")
+    kv.kvpop_future_attn_target(q, k, w.scale, 0, -1, lse_ws=lse, out=out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().astype(np.float64)
+    assert np.all(np.isfinite(got))
+    np.testing.assert_allclose(got.sum(axis=-1), T, rtol=REL)
+    for b, qh in [(0, 0), (B - 1, H - 1)]:
+        lse_ref = oracle.row_lse_blocked(w.q_bits[b, qh], w.k_bits[b, qh], w.scale)
+        _check_lse(lse[b, qh].cpu().numpy().astype(np.float64), lse_ref, "batches b%d h%d" % (b, qh))
+        ref = oracle.future_mass_blocked(w.q_bits[b, qh], w.k_bits[b, qh], w.scale, None, 0, -1, lse=lse_ref)
+        _check_out(got[b, qh], ref, 0, "batches b%d h%d" % (b, qh))
+
+
 def test_qwen3_8b_t32k_one_head_exhaustive():
     """One (b, query head) of the T=32768 workload, every key, blocked oracle."""
     b, qh = 2, 6
