@@ -604,27 +604,45 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
       }
     };
 
-    // Tile on a band edge: mask each pair by window <= i - j <= hz.
+    // Tile on a band edge. Each key subtile of the wave is classified once: outside
+    // the band (skipped), inside it (summed without a mask) or across its edge (each
+    // pair masked by window <= i - j <= hz).
     auto edge_step = [&](const uint16_t* sq, const float* sl, int i0) __attribute__((always_inline)) {
+      bool act[NS], inside[NS];
+#pragma unroll
+      for (int n = 0; n < NS; ++n) {
+        const int dlo = i0 - (jw + 32 * n + 31), dhi = i0 + 31 - (jw + 32 * n);
+        act[n] = !(dhi < window || dlo > hz);
+        inside[n] = dlo >= window && dhi <= hz;
+      }
 #pragma unroll
       for (int g = 0; g < GC; ++g) {
         float nl[16];
         read_nl(sl, g, nl);
 #pragma unroll
         for (int n = 0; n < NS; ++n) {
+          if (!act[n]) continue;
           f32x16 acc = f32x16{};
 #pragma unroll
           for (int ks = 0; ks < KS; ++ks) acc = mfma32(TL::frag(sq + g * TL::ELEMS, lane, ks), kf[n][ks], acc);
-          const int base = i0 + 4 * hi - (jw + 32 * n + l32);
-          float ts = 0.f;
+          float ts[2];
+          if (inside[n]) {
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int d = base + 8 * (r >> 2) + (r & 3);
-            const float e = exp2_fast(__builtin_fmaf(acc[r], c, nl[r]));
-            const float x = (d >= window && d <= hz) ? e : 0.f;
-            ts = r == 0 ? x : ts + x;  // the first term seeds the sum
+            for (int r = 0; r < 16; ++r) {
+              const float x = exp2_fast(__builtin_fmaf(acc[r], c, nl[r]));
+              ts[r & 1] = r < 2 ? x : ts[r & 1] + x;  // the first terms seed the sums
+            }
+          } else {
+            const int base = i0 + 4 * hi - (jw + 32 * n + l32);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const int d = base + 8 * (r >> 2) + (r & 3);
+              const float e = exp2_fast(__builtin_fmaf(acc[r], c, nl[r]));
+              const float x = (d >= window && d <= hz) ? e : 0.f;
+              ts[r & 1] = r < 2 ? x : ts[r & 1] + x;
+            }
           }
-          colsum[g][n] += ts;
+          colsum[g][n] += ts[0] + ts[1];
         }
       }
     };
