@@ -254,6 +254,15 @@ def test_groups_taken_in_batches_per_xcd():
         _check_lse(lse[b, qh].cpu().numpy().astype(np.float64), lse_ref, "batches b%d h%d" % (b, qh))
         ref = oracle.future_mass_blocked(w.q_bits[b, qh], w.k_bits[b, qh], w.scale, None, 0, -1, lse=lse_ref)
         _check_out(got[b, qh], ref, 0, "batches b%d h%d" % (b, qh))
+    # The fused epilogue takes the same launch order; with one query head per KV head
+    # its mean score is log(mass + eps) - log N_t of that head's own masses.
+    sc = torch.full((B, H, T), float("nan"), device="cuda")
+    kv.kvpop_future_attn_scores(q, k, lse, w.scale, 0, -1, agg="mean", eps=1e-8, normalize=True, scores=sc)
+    torch.cuda.synchronize()
+    sc = sc.cpu().numpy().astype(np.float64)
+    assert np.all(np.isfinite(sc))
+    want = oracle.target_scores(got, H, 0, -1, "mean", 1e-8)
+    assert np.abs(sc - want).max() <= 1e-5
 
 
 def test_qwen3_8b_t32k_one_head_exhaustive():
