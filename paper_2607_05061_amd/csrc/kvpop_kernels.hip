@@ -124,10 +124,12 @@ __device__ __forceinline__ void load_b_operand(bf16x8 (&f)[D / 16], const uint16
 // are visited diagonal-first: the tiles that straddle the diagonal (and any step
 // that shares them) update (m, sum) exactly, as in online softmax. Every later
 // step lies strictly below the diagonal and takes the exponentials against the
-// current m with no per-element maximum; a lane whose tile sum exceeds 2^64 (a
-// logit more than 64 log2-units above m, or inf) flags the step, which is then
-// redone exactly from the LDS tiles. The result is the same LSE; the common path
-// costs one fma, one exp and one add per pair.
+// current m with no per-element maximum; a lane whose running sum exceeds 2^64
+// after the step flags it, and the step is then redone exactly from the LDS tiles.
+// Any term above 2^64 (a logit more than 64 log2-units above m, or inf) raises the
+// sum past that bound; a sum that gets there from smaller terms only costs a redo.
+// The result is the same LSE; the common path costs one fma, one exp and one add
+// per pair.
 // ---------------------------------------------------------------------------
 template <int D, int P, bool HAS_BIAS>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2))) void
@@ -321,15 +323,13 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
       }
       if (u > 0) {
 #pragma unroll
-        for (int n = 0; n < NQ; ++n) {
-          const float t = ts[n][0] + ts[n][1];
-          sum[n] += t;
-          ovf |= !(t <= kOverflow);
-        }
+        for (int n = 0; n < NQ; ++n) sum[n] += ts[n][0] + ts[n][1];
       }
 #pragma unroll
       for (int n = 0; n < NQ; ++n) acc_prev[n] = acc[n];
     }
+#pragma unroll
+    for (int n = 0; n < NQ; ++n) ovf |= !(sum[n] <= kOverflow);
     return ovf;
   };
 
