@@ -389,7 +389,8 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
 // its 16 query rows of each tile into a per-tile sum and then into a running
 // column sum (a two-level sum keeps the fp32 error near (16 + tiles) ulp). At the
 // end the two half-wave sums of each column are added and written: each workgroup
-// owns its output columns, so no atomics are needed and results are deterministic.
+// owns its output columns, so results are deterministic. (A split launch, for
+// small grids, adds exactly two partial sums per column into a zeroed output.)
 //
 // Query rows beyond T get LSE = +inf in LDS, which zeroes their terms. A per-key
 // bias is factored out of the sum, out_t = exp(bias_t) * sum_d exp(...). Query
@@ -406,7 +407,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_pe
 future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const float* __restrict__ bias,
                    const float* __restrict__ lse, float* __restrict__ out, int B, int Hq, int Hkv, int T, float c,
                    int window, int hz, float* __restrict__ scores, int agg_mean, float eps, int normalize,
-                   int xgroups) {
+                   int xgroups, int split) {
   using TL = Tile<D>;
   constexpr int KS = TL::KS;
   constexpr int WK = NS * 32;  // keys per wave
@@ -428,8 +429,17 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
   // of groups heaviest key block first: more workgroups of one group then sweep
   // the same query tiles together and share them in that XCD's L2. Otherwise the
   // order is key block major, heaviest first, over all groups.
-  int kb, bh;
-  if (xgroups > 0) {
+  // A split launch (a small grid, no epilogue) gives each half of a key block's
+  // sweep its own workgroup, heaviest block first; the two halves add their partial
+  // sums into the zero-filled output, and a + b = b + a keeps the result exact to
+  // the bit whichever lands first.
+  int kb, bh, half = 0;
+  if (split) {
+    const int u = blockIdx.x / nbh;
+    kb = u >> 1;
+    half = u & 1;
+    bh = blockIdx.x - u * nbh;
+  } else if (xgroups > 0) {
     const int nkb = (T + BK - 1) / BK;
     const int x = (int)(blockIdx.x & 7), j = (int)(blockIdx.x >> 3);
     const int span = xgroups * nkb;
@@ -453,6 +463,9 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     qt_hi = (int)(r_hi / 32);
     nqt = qt_hi - (int)(r_lo / 32) + 1;
   }
+  // The steps of the sweep this workgroup takes (its half in a split launch).
+  const int s_begin = split && half ? nqt / 2 : 0;
+  const int s_end = split && !half ? nqt / 2 : nqt;
 
   float fac[NS];
 #pragma unroll
@@ -648,7 +661,7 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     };
 
     auto step = [&](int s, const uint16_t* sq, const float* sl, uint16_t* nsq, float* nsl) __attribute__((always_inline)) {
-      const bool more = s + 1 < nqt;
+      const bool more = s + 1 < s_end;
       if (more) issue(s + 1, nsq);
       const int i0 = (qt_hi - s) * 32;
       // Differences d = i - j over this wave's keys and the tile's rows.
@@ -663,12 +676,14 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
       __syncthreads();
     };
 
-    issue(0, sq0);
-    commit(sl0);
-    __syncthreads();
-    for (int s = 0; s < nqt; s += 2) {
-      step(s, sq0, sl0, sq1, sl1);
-      if (s + 1 < nqt) step(s + 1, sq1, sl1, sq0, sl0);
+    if (s_begin < s_end) {
+      issue(s_begin, sq0);
+      commit(sl0);
+      __syncthreads();
+      for (int s = s_begin; s < s_end; s += 2) {
+        step(s, sq0, sl0, sq1, sl1);
+        if (s + 1 < s_end) step(s + 1, sq1, sl1, sq0, sl0);
+      }
     }
 
     // Combine the half-wave sums and write this chunk's columns.
@@ -679,12 +694,20 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
         float v = colsum[g][n] + __shfl_xor(colsum[g][n], 32);
         if (HAS_BIAS) v *= fac[n];
         const int j = jw + 32 * n + l32;
-        if (hi == 0 && j < T && (!EPI || out)) out[(head0 + g) * T + j] = v;
+        if (hi == 0 && j < T && (!EPI || out)) {
+          if (!EPI && split) atomicAdd(&out[(head0 + g) * T + j], v);
+          else out[(head0 + g) * T + j] = v;
+        }
         if (EPI) aggv[n] = agg_mean ? aggv[n] + v : fmaxf(aggv[n], v);
       }
     }
   }
   if (EPI) write_scores();
+}
+
+// Zeroes n floats (the output of a split pass-2 launch).
+__global__ __launch_bounds__(256) void zero_fill_kernel(float* __restrict__ p, long long n) {
+  for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < n; i += (long long)gridDim.x * 256) p[i] = 0.f;
 }
 
 template <int D, int P, bool HB>
@@ -731,10 +754,22 @@ int launch_p2(const Launch& L) {
     const int ng = nbh / 8;
     xgroups = ng % 2 == 0 && (long long)ng * nkb >= 4 * 64 ? ng / 2 : ng;
   }
-  hipLaunchKernelGGL((future_mass_kernel<D, NS, GC, HB, EPI>), dim3((unsigned)grid), dim3(256), 0,
-                     (hipStream_t)L.stream, reinterpret_cast<const uint16_t*>(L.q),
+  // Under 1024 workgroups (4 per CU) the heaviest key blocks set the time: split
+  // every block's sweep in two, into a zero-filled output (not with the epilogue,
+  // which needs each key's whole mass).
+  const int split = !EPI && grid < 1024;
+  if (split) {
+    const long long n = (long long)L.B * L.Hq * L.T;
+    const long long fg = (n + 255) / 256;
+    hipLaunchKernelGGL(zero_fill_kernel, dim3((unsigned)(fg < 4096 ? fg : 4096)), dim3(256), 0,
+                       (hipStream_t)L.stream, L.out, n);
+    const int e = (int)hipGetLastError();
+    if (e) return e;
+  }
+  hipLaunchKernelGGL((future_mass_kernel<D, NS, GC, HB, EPI>), dim3((unsigned)(split ? 2 * grid : grid)), dim3(256),
+                     0, (hipStream_t)L.stream, reinterpret_cast<const uint16_t*>(L.q),
                      reinterpret_cast<const uint16_t*>(L.k), L.bias, L.lse, L.out, L.B, L.Hq, L.Hkv, L.T, c, L.window,
-                     hz, L.scores, L.agg, L.eps, L.normalize, xgroups);
+                     hz, L.scores, L.agg, L.eps, L.normalize, split ? 0 : xgroups, split);
   return (int)hipGetLastError();
 }
 

@@ -70,8 +70,11 @@ def test_scores_match_oracle(case, agg):
         got, out, mass = _scores(w, win, hor, agg, eps, normalize, write_mass=True)
         ref = oracle.target_scores(m_ref, Hkv, win, hor, agg=agg, eps=eps, normalize=normalize)
         _check(got, ref, "case %s agg %s eps %g norm %s" % (case, agg, eps, normalize))
-        # the per-head masses written by the fused kernel are the plain pass-2 masses
-        np.testing.assert_array_equal(out, mass)
+        # the per-head masses written by the fused kernel are the plain pass-2 masses,
+        # up to the fp32 summation order: a launch this small splits each key block's
+        # sweep of plain pass 2 in two halves, added at the end (the fused kernel
+        # never splits, since it needs each key's whole mass)
+        np.testing.assert_allclose(out, mass, rtol=1e-5, atol=0)
 
 
 def test_scores_with_sink_and_masked_keys():
