@@ -754,10 +754,10 @@ int launch_p2(const Launch& L) {
     const int ng = nbh / 8;
     xgroups = ng % 2 == 0 && (long long)ng * nkb >= 4 * 64 ? ng / 2 : ng;
   }
-  // Under 1024 workgroups (4 per CU) the heaviest key blocks set the time: split
+  // Under 2048 workgroups (8 per CU) the heaviest key blocks set the time: split
   // every block's sweep in two, into a zero-filled output (not with the epilogue,
   // which needs each key's whole mass).
-  const int split = !EPI && grid < 1024;
+  const int split = !EPI && grid < 2048;
   if (split) {
     const long long n = (long long)L.B * L.Hq * L.T;
     const long long fg = (n + 255) / 256;
