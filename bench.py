@@ -87,35 +87,57 @@ def traffic_for(kernel: str, workload: str):
     return k.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(w, band):
-    """The fp64 oracle, as it stands, on one (batch row, KV head) group of the same
-    workload: its G query heads, row LSE then future mass."""
-    import numpy as np
-    import oracle
+def host_cores():
+    """os.cpu_count(), the CPUs this process may run on (what `nproc` prints), and
+    the BLAS library's thread count."""
     try:
         from threadpoolctl import threadpool_info
-        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+        blas = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
     except Exception:  # pragma: no cover
-        blas_threads = 1
-    b, h = 0, 0
-    k = w.k_bits[b, h]
+        blas = 1
+    return os.cpu_count() or 1, len(os.sched_getaffinity(0)), int(blas)
+
+
+def cpu_baseline(w, band, min_seconds: float = 10.0):
+    """The fp64 oracle, as it stands, on (batch row, KV head) groups of the same
+    workload, taken in order until at least ``min_seconds`` have passed: per group
+    its G query heads, row LSE then future mass, in the oracle's blocked form with
+    its row blocks on every CPU this process may use."""
+    import numpy as np
+    import oracle
+    n_cpu, n_proc, blas = host_cores()
+    threads = n_proc
     T = w.T
+    groups = 0
     t0 = time.perf_counter()
-    for g in range(w.G):
-        q = w.q_bits[b, h * w.G + g]
-        lse = oracle.row_lse_blocked(q, k, w.scale, w.bias)
-        out = oracle.future_mass_blocked(q, k, w.scale, w.bias, band[0], band[1], lse=lse)
-        assert np.isfinite(out).all()
+    for b in range(w.B):
+        for h in range(w.Hkv):
+            k = w.k_bits[b, h]
+            for g in range(w.G):
+                q = w.q_bits[b, h * w.G + g]
+                lse = oracle.row_lse_blocked(q, k, w.scale, w.bias, block=512, threads=threads)
+                out = oracle.future_mass_blocked(q, k, w.scale, w.bias, band[0], band[1], lse=lse, block=512,
+                                                 threads=threads)
+                assert np.isfinite(out).all()
+            groups += 1
+            if time.perf_counter() - t0 >= min_seconds:
+                break
+        if time.perf_counter() - t0 >= min_seconds:
+            break
     dt = time.perf_counter() - t0
-    pairs = w.G * T * (T + 1) // 2
+    pairs = groups * w.G * T * (T + 1) // 2
     return {
         "value": pairs / dt,
         "unit": "pairs/s",
-        "cores": int(blas_threads),
+        "cores": int(threads),
         "kind": "oracle",
-        "sample": "one (b=0, kv head 0) group of %s: %d query heads x T(T+1)/2 = %d pairs, row LSE then future "
-                  "mass with band %s; fp64 numpy, blocked 1024-row form (BLAS on %d threads, elementwise ops on "
-                  "one); %.1f s" % (w.name, w.G, pairs, tuple(band), blas_threads, dt),
+        "os_cpu_count": int(n_cpu),
+        "nproc": int(n_proc),
+        "blas_threads": int(blas),
+        "sample": "the first %d (b, kv head) group(s) of %s: %d query heads each, %d pairs in all (every causal "
+                  "pair once), row LSE then future mass with band %s; fp64 numpy oracle, blocked 512-row form, "
+                  "row blocks on %d host threads (BLAS held to one thread per block); %.1f s"
+                  % (groups, w.name, w.G, pairs, tuple(band), threads, dt),
     }
 
 

@@ -32,9 +32,11 @@
  *    row-major device memory (bf16 = IEEE binary32 with the low 16 bits dropped).
  *    Query head qh reads KV head qh / G (contiguous query-head groups).
  *  - key_bias is an optional fp32 [T] device array (NULL = no bias), shared by all
- *    batch rows and heads. Values may be -INFINITY (key never attended). Finite
- *    values must be >= -80: pass 2 factors exp(key_bias[t]) out of each key's sum,
- *    and below that bound the factored sum may overflow.
+ *    batch rows and heads. Values are finite or -INFINITY (key never attended: its
+ *    mass is exactly 0); NaN and +INFINITY are not supported. Pass 2 factors
+ *    exp(key_bias[t]) out of key t's sum when |key_bias[t]| <= 30 and otherwise
+ *    adds the bias to every exponent of a guarded sweep, so any finite bias is
+ *    exact to the tolerance.
  *  - lse is fp32 [B, Hq, T] holding natural-log normalisers; out is fp32
  *    [B, Hq, T] holding the linear (not log) unnormalised future mass. Keys whose
  *    band is empty (t + window > T - 1) get exactly 0.
@@ -99,9 +101,16 @@ int kvpop_row_lse(const kvpop_dims* dims, const void* q, const void* k, const fl
  * future_mass_app, App. D.2):
  *   out[b, qh, t] = sum_{d in band(t)} exp(l(d, t) - lse[b, qh, d]).
  * lse is normally the output of kvpop_row_lse on the same q, k, key_bias, which
- * makes every summand a probability (<= 1). With any other normaliser (e.g. the
- * sparse one of App. D.3) the caller must ensure l(d, t) - lse[d] stays below
- * about 88 for admissible pairs, or the sums overflow to +inf.
+ * makes every summand a probability (<= 1). Any other normaliser is accepted,
+ * such as the sparse one of Sec. 3.2 eq. sparse_lse_main / App. D.3, which lies
+ * below the dense one, so that summands of keys outside its mask exceed 1 without
+ * bound. Guard: a workgroup whose fast sweep leaves a column sum above 2^64 (or
+ * inf / NaN) recomputes its key block with a per-column running maximum. out is
+ * then the fp32 rounding of the mass (within the relative 2e-3 bar), +INFINITY
+ * where the mass exceeds the fp32 range (for example lse[d] = -INFINITY for an
+ * admissible d), exactly 0 for keys biased -INFINITY. lse must not be NaN. Masses
+ * below about 1e-30 lie in or near fp32's subnormal range and carry no relative
+ * accuracy.
  * window >= 0; horizon < 0 (unbounded) or horizon >= window. out: fp32 [B,Hq,T]. */
 int kvpop_future_attn_from_lse(const kvpop_dims* dims, const void* q, const void* k,
                                const float* key_bias, const float* lse, int32_t window,

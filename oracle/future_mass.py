@@ -17,6 +17,8 @@ length T.
 """
 from __future__ import annotations
 
+import concurrent.futures as _cf
+
 import numpy as np
 
 __all__ = [
@@ -171,29 +173,43 @@ def _check_band(window: int, horizon: int) -> None:
 # (b, KV head) slices at the benchmark sizes.
 # ---------------------------------------------------------------------------
 
-def _block_logits(q_blk: np.ndarray, d0: int, k: np.ndarray, scale: float, bias) -> np.ndarray:
-    """Logits for query rows d0..d0+n-1 against keys 0..d0+n-1 (causally masked)."""
+def _block_logits(q_blk: np.ndarray, d0: int, k: np.ndarray, scale: float, bias, t0: int = 0) -> np.ndarray:
+    """Logits for query rows d0..d0+n-1 against keys t0..d0+n-1 (causally masked)."""
     n = q_blk.shape[0]
-    kk = k[: d0 + n]
+    kk = k[t0: d0 + n]
     L = float(scale) * (q_blk @ kk.T)
     if bias is not None:
-        L = L + bias[None, : d0 + n]
+        L = L + bias[None, t0: d0 + n]
     d = d0 + np.arange(n)[:, None]
-    t = np.arange(d0 + n)[None, :]
+    t = t0 + np.arange(d0 + n - t0)[None, :]
     L[t > d] = -np.inf
     return L
 
 
-def row_lse_blocked(q, k, scale: float, bias=None, block: int = 1024) -> np.ndarray:
-    """LSE_d for one head (q [T,D], k [T,D]), one block of query rows at a time."""
+def _map_blocks(fn, starts, threads: int):
+    """fn over row-block starts, in order; on ``threads`` host threads when > 1
+    (NumPy's elementwise ufuncs and BLAS release the GIL; BLAS is then held to one
+    thread per block so the two levels of threading do not multiply)."""
+    if threads <= 1 or len(starts) <= 1:
+        return [fn(d0) for d0 in starts]
+    from threadpoolctl import threadpool_limits
+    with threadpool_limits(1, user_api="blas"), _cf.ThreadPoolExecutor(threads) as ex:
+        return list(ex.map(fn, starts))
+
+
+def row_lse_blocked(q, k, scale: float, bias=None, block: int = 1024, threads: int = 1) -> np.ndarray:
+    """LSE_d for one head (q [T,D], k [T,D]), one block of query rows at a time
+    (blocks are independent; ``threads`` > 1 evaluates them on that many host threads)."""
     q = _as_f64(q)
     k = _as_f64(k)
     bias = None if bias is None else _as_f64(bias)
     T = q.shape[0]
     out = np.empty(T)
-    for d0 in range(0, T, block):
-        L = _block_logits(q[d0:d0 + block], d0, k, scale, bias)
-        out[d0:d0 + block] = _lse_rows_of(L)
+
+    def one(d0):
+        out[d0:d0 + block] = _lse_rows_of(_block_logits(q[d0:d0 + block], d0, k, scale, bias))
+
+    _map_blocks(one, list(range(0, T, block)), threads)
     return out
 
 
@@ -213,29 +229,38 @@ def row_lse_rows(q, k, scale: float, rows, bias=None) -> np.ndarray:
 
 
 def future_mass_blocked(q, k, scale: float, bias=None, window: int = 0, horizon: int = -1,
-                        lse=None, block: int = 1024) -> np.ndarray:
+                        lse=None, block: int = 1024, threads: int = 1) -> np.ndarray:
     """m_bar_t for one head, accumulating column sums one block of query rows at a time.
 
     Same definition as ``future_mass`` (eq. future_mass_app). ``lse`` (length T)
-    defaults to ``row_lse_blocked``.
+    defaults to ``row_lse_blocked``. With a finite horizon a block of rows d0.. only
+    reaches keys t >= d0 - horizon, so earlier keys are not evaluated. The blocks'
+    column sums are added in block order; ``threads`` > 1 evaluates the blocks on
+    that many host threads.
     """
     _check_band(window, horizon)
     q = _as_f64(q)
     k = _as_f64(k)
     bias = None if bias is None else _as_f64(bias)
     T = q.shape[0]
-    lse_d = row_lse_blocked(q, k, scale, bias, block) if lse is None else np.asarray(lse, np.float64)
-    out = np.zeros(T)
-    for d0 in range(0, T, block):
+    lse_d = row_lse_blocked(q, k, scale, bias, block, threads) if lse is None else np.asarray(lse, np.float64)
+
+    def one(d0):
         n = min(block, T - d0)
-        L = _block_logits(q[d0:d0 + n], d0, k, scale, bias)
+        t0 = 0 if horizon < 0 else max(0, d0 - horizon)
+        L = _block_logits(q[d0:d0 + n], d0, k, scale, bias, t0)
         P = np.exp(L - lse_d[d0:d0 + n, None])
         d = d0 + np.arange(n)[:, None]
-        t = np.arange(d0 + n)[None, :]
+        t = t0 + np.arange(d0 + n - t0)[None, :]
         ok = d >= t + window
         if horizon >= 0:
             ok &= d <= t + horizon
-        out[: d0 + n] += np.sum(np.where(ok, P, 0.0), axis=0)
+        return t0, np.sum(np.where(ok, P, 0.0), axis=0)
+
+    out = np.zeros(T)
+    starts = list(range(0, T, block))
+    for d0, (t0, part) in zip(starts, _map_blocks(one, starts, threads)):
+        out[t0: t0 + part.shape[0]] += part
     return out
 
 

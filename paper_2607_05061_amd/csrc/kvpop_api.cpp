@@ -6,6 +6,7 @@
 #include <hip/hip_runtime_api.h>
 
 #include <cmath>
+#include <cstdlib>
 #include <cstdint>
 #include <string>
 
@@ -62,6 +63,24 @@ int hip_status(int e) {
   if (e == 0) return KVPOP_OK;
   g_err_text = std::string("HIP error: ") + hipGetErrorString(static_cast<hipError_t>(e));
   return KVPOP_EHIP;
+}
+
+// Test hook for the KVPOP_EHIP path: with the environment variable
+// KVPOP_TEST_FORCE_EHIP set to a nonzero hipError_t code, every entry point fails
+// after validation as if its first launch had returned that code, and launches
+// nothing. Unset (the normal case) it costs one getenv per call.
+int forced_hip_error() {
+  const char* e = std::getenv("KVPOP_TEST_FORCE_EHIP");
+  return e ? std::atoi(e) : 0;
+}
+
+// Runs the launches of one entry point (a callable returning 0 or the hipError_t
+// of the launch that failed) and maps the result to a status.
+template <class F>
+int launch(F&& f) {
+  const int forced = forced_hip_error();
+  if (forced != 0) return hip_status(forced);
+  return hip_status(f());
 }
 
 kvpop::Launch make_launch(const kvpop_dims* d, const void* q, const void* k, const float* bias, void* stream) {
@@ -130,7 +149,7 @@ int kvpop_row_lse(const kvpop_dims* dims, const void* q, const void* k, const fl
   if (st != KVPOP_OK) return st;
   kvpop::Launch L = make_launch(dims, q, k, key_bias, stream);
   L.out = lse;
-  return hip_status(kvpop::launch_row_lse(L));
+  return launch([&] { return kvpop::launch_row_lse(L); });
 }
 
 int kvpop_future_attn_from_lse(const kvpop_dims* dims, const void* q, const void* k, const float* key_bias,
@@ -149,7 +168,7 @@ int kvpop_future_attn_from_lse(const kvpop_dims* dims, const void* q, const void
   L.out = out;
   L.window = window;
   L.horizon = horizon;
-  return hip_status(kvpop::launch_future_mass(L));
+  return launch([&] { return kvpop::launch_future_mass(L); });
 }
 
 int kvpop_future_attn_scores(const kvpop_dims* dims, const void* q, const void* k, const float* key_bias,
@@ -182,7 +201,7 @@ int kvpop_future_attn_scores(const kvpop_dims* dims, const void* q, const void* 
   L.agg = agg;
   L.eps = eps;
   L.normalize = normalize;
-  return hip_status(kvpop::launch_future_mass(L));
+  return launch([&] { return kvpop::launch_future_mass(L); });
 }
 
 size_t kvpop_running_topk_workspace_size(const kvpop_topk_dims* d) {
@@ -236,7 +255,7 @@ int kvpop_running_topk(const kvpop_topk_dims* d, const float* scores, const floa
   L.evict = evict;
   L.workspace = workspace;
   L.stream = stream;
-  return hip_status(kvpop::launch_running_topk(L));
+  return launch([&] { return kvpop::launch_running_topk(L); });
 }
 
 int kvpop_sparse_attn_fwd(const kvpop_dims* dims, const void* q, const void* k, const void* v,
@@ -273,7 +292,7 @@ int kvpop_sparse_attn_fwd(const kvpop_dims* dims, const void* q, const void* k, 
   L.D = dims->head_dim;
   L.scale = dims->scale;
   L.stream = stream;
-  return hip_status(kvpop::launch_sparse_attn_fwd(L));
+  return launch([&] { return kvpop::launch_sparse_attn_fwd(L); });
 }
 
 int kvpop_future_attn_target(const kvpop_dims* dims, const void* q, const void* k, const float* key_bias,
@@ -288,14 +307,16 @@ int kvpop_future_attn_target(const kvpop_dims* dims, const void* q, const void* 
   st = check_output(out, sz.row_elems * 4, sz, dims, q, k, key_bias, lse_ws, sz.row_elems * 4);
   if (st != KVPOP_OK) return st;
   kvpop::Launch L = make_launch(dims, q, k, key_bias, stream);
-  L.out = lse_ws;
-  st = hip_status(kvpop::launch_row_lse(L));
-  if (st != KVPOP_OK) return st;
-  L.lse = lse_ws;
-  L.out = out;
-  L.window = window;
-  L.horizon = horizon;
-  return hip_status(kvpop::launch_future_mass(L));
+  return launch([&] {
+    L.out = lse_ws;
+    const int e = kvpop::launch_row_lse(L);
+    if (e != 0) return e;
+    L.lse = lse_ws;
+    L.out = out;
+    L.window = window;
+    L.horizon = horizon;
+    return kvpop::launch_future_mass(L);
+  });
 }
 
 }  // extern "C"

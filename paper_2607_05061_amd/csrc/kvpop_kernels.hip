@@ -40,6 +40,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+
 #include "kvpop_internal.h"
 
 namespace kvpop {
@@ -57,6 +58,9 @@ constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kMaxFloor = -1.0e38f;
 // A tile's partial sum above this means the reference maximum was too low.
 constexpr float kOverflow = 18446744073709551616.0f;  // 2^64
+// Pass 2 factors exp(bias_t) out of key t's sum only for |bias_t| <= kBiasFast
+// (natural-log units); larger finite biases take the exact sweep.
+constexpr float kBiasFast = 30.0f;
 // Buffer descriptor word 3 for raw (untyped) gfx9 buffer access.
 constexpr int kRsrcWord3 = 0x00020000;
 
@@ -396,6 +400,19 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
 // bias is factored out of the sum, out_t = exp(bias_t) * sum_d exp(...). Query
 // heads are processed GC at a time; G / GC chunks each repeat the sweep.
 //
+// Guard. The fast sweep sums exp2(x) against the fixed reference 0, which is safe
+// when every summand is a probability (the dense normaliser) and the factored bias
+// is moderate. A caller-supplied normaliser may be smaller than the dense one (the
+// sparse normaliser of App. D.3), so summands can exceed 1 without bound; a large
+// bias makes the factored sum overflow or underflow. So: a workgroup whose keys
+// carry a finite bias beyond +-kBiasFast runs the exact sweep from the start, and
+// after a fast sweep any column sum above 2^64 (or inf / NaN) sends the whole
+// workgroup through the exact sweep again. The exact sweep keeps, per column, a
+// running maximum m of the summands' exponents (bias included) and the sum
+// relative to it, rescaled whenever m grows, and writes exp2(m + log2 sum): the
+// fp32 rounding of the mass, +inf only when the mass itself exceeds the fp32 range.
+// Keys with bias -inf are never attended and get exactly 0.
+//
 // With EPI the kernel also finishes the target (App. D.4 step 5, App. B.1-B.2):
 // it folds the G per-head masses of each key into their max or sum as the chunks
 // complete, and writes log(agg + eps) - log N_t per KV head, where N_t = max(1,
@@ -407,7 +424,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_pe
 future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const float* __restrict__ bias,
                    const float* __restrict__ lse, float* __restrict__ out, int B, int Hq, int Hkv, int T, float c,
                    int window, int hz, float* __restrict__ scores, int agg_mean, float eps, int normalize,
-                   int xgroups, int split) {
+                   int xgroups, int split, int hs) {
   using TL = Tile<D>;
   constexpr int KS = TL::KS;
   constexpr int WK = NS * 32;  // keys per wave
@@ -433,12 +450,20 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
   // sweep its own workgroup, heaviest block first; the two halves add their partial
   // sums into the zero-filled output, and a + b = b + a keeps the result exact to
   // the bit whichever lands first.
-  int kb, bh, half = 0;
+  int kb, bh, half = 0, ch = 0;
   if (split) {
     const int u = blockIdx.x / nbh;
     kb = u >> 1;
     half = u & 1;
     bh = blockIdx.x - u * nbh;
+  } else if (hs > 1) {
+    // Head-split launch: hs workgroups per (key block, group), workgroup ch taking
+    // the head chunks ch, ch + hs, ...; key block major, heaviest first.
+    const int per = nbh * hs;
+    kb = blockIdx.x / per;
+    const int r = blockIdx.x - kb * per;
+    bh = r / hs;
+    ch = r - bh * hs;
   } else if (xgroups > 0) {
     const int nkb = (T + BK - 1) / BK;
     const int x = (int)(blockIdx.x & 7), j = (int)(blockIdx.x >> 3);
@@ -467,14 +492,23 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
   const int s_begin = split && half ? nqt / 2 : 0;
   const int s_end = split && !half ? nqt / 2 : nqt;
 
-  float fac[NS];
+  // Bias of this lane's key columns: factored out (fac) by the fast sweep, added to
+  // every exponent (bl2, log2 units) by the exact sweep. masked: bias -inf.
+  float fac[NS], bl2[NS];
+  bool masked[NS];
+  bool big = false;
 #pragma unroll
   for (int n = 0; n < NS; ++n) {
     fac[n] = 1.f;
+    bl2[n] = 0.f;
+    masked[n] = false;
     if (HAS_BIAS) {
       const int j = min(jw + 32 * n + l32, T - 1);
       const float bj = bias[j];
-      fac[n] = bj == -__builtin_inff() ? 0.f : exp2_fast(bj * kLog2e);
+      masked[n] = bj == -__builtin_inff();
+      bl2[n] = masked[n] ? 0.f : bj * kLog2e;
+      fac[n] = masked[n] ? 0.f : exp2_fast(bl2[n]);
+      big |= !masked[n] && !(__builtin_fabsf(bj) <= kBiasFast);
     }
   }
 
@@ -511,6 +545,9 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     return;
   }
 
+  // Workgroup-uniform: any key of the block with a large finite bias.
+  const bool all_exact = HAS_BIAS && __syncthreads_or(big);
+
   bf16x8 kf[NS][KS];  // this lane's key rows (B operand), resident for the whole sweep
   const uint16_t* Kbh = K + (size_t)bh * T * D;
 #pragma unroll
@@ -520,7 +557,7 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
   const int pg = (w * PPW) / KS;          // the head tile this wave copies
   const int ps0 = (w * PPW) - pg * KS;    // its first plane
 
-  for (int gh0 = h * G; gh0 < (h + 1) * G; gh0 += GC) {
+  for (int gh0 = h * G + ch * GC; gh0 < (h + 1) * G; gh0 += GC * hs) {
     const size_t head0 = (size_t)(b * Hq + gh0);
     float stl = 0.f;
     // Start the loads of step s: Q tiles straight into LDS, raw LSE into a register.
@@ -537,11 +574,8 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
       if (tid < GC * 32) sl[tid] = -stl * kLog2e;
     };
 
-    float colsum[GC][NS];
-#pragma unroll
-    for (int g = 0; g < GC; ++g)
-#pragma unroll
-      for (int n = 0; n < NS; ++n) colsum[g][n] = 0.f;
+    float colsum[GC][NS];  // fast sweep: column sums; exact sweep: sums relative to mref
+    float mref[GC][NS];    // exact sweep: running maximum of the exponents (log2 units)
 
     auto read_nl = [&](const float* sl, int g, float (&nl)[16]) {
 #pragma unroll
@@ -660,6 +694,51 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
       }
     };
 
+    // Exact step (guarded sweep): every admissible pair's exponent x = acc * c -
+    // LSE_d log2 e + bias_t log2 e, and per column an online update of (mref, colsum)
+    // as in online softmax. A summand of +inf (LSE_d = -inf) makes the mass +inf.
+    auto exact_step = [&](const uint16_t* sq, const float* sl, int i0) __attribute__((always_inline)) {
+      bool act[NS];
+#pragma unroll
+      for (int n = 0; n < NS; ++n) {
+        const int dlo = i0 - (jw + 32 * n + 31), dhi = i0 + 31 - (jw + 32 * n);
+        act[n] = !(dhi < window || dlo > hz);
+      }
+#pragma unroll
+      for (int g = 0; g < GC; ++g) {
+        float nl[16];
+        read_nl(sl, g, nl);
+#pragma unroll
+        for (int n = 0; n < NS; ++n) {
+          if (!act[n]) continue;
+          f32x16 acc = f32x16{};
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) acc = mfma32(TL::frag(sq + g * TL::ELEMS, lane, ks), kf[n][ks], acc);
+          const int base = i0 + 4 * hi - (jw + 32 * n + l32);
+          float x[16];
+          float tmax = -__builtin_inff();
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int d = base + 8 * (r >> 2) + (r & 3);
+            const float xr = __builtin_fmaf(acc[r], c, nl[r]) + bl2[n];
+            x[r] = (d >= window && d <= hz) ? xr : -__builtin_inff();
+            tmax = fmaxf(tmax, x[r]);
+          }
+          const float mn = fmaxf(mref[g][n], tmax);
+          if (mn == __builtin_inff()) {
+            mref[g][n] = mn;
+            colsum[g][n] = 1.f;
+          } else if (mn > -__builtin_inff()) {
+            float e = 0.f;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) e += exp2_fast(x[r] - mn);
+            colsum[g][n] = colsum[g][n] * exp2_fast(mref[g][n] - mn) + e;
+            mref[g][n] = mn;
+          }
+        }
+      }
+    };
+
     auto step = [&](int s, const uint16_t* sq, const float* sl, uint16_t* nsq, float* nsl) __attribute__((always_inline)) {
       const bool more = s + 1 < s_end;
       if (more) issue(s + 1, nsq);
@@ -676,29 +755,97 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
       __syncthreads();
     };
 
-    if (s_begin < s_end) {
-      issue(s_begin, sq0);
-      commit(sl0);
-      __syncthreads();
-      for (int s = s_begin; s < s_end; s += 2) {
-        step(s, sq0, sl0, sq1, sl1);
-        if (s + 1 < s_end) step(s + 1, sq1, sl1, sq0, sl0);
+#pragma unroll
+    for (int g = 0; g < GC; ++g)
+#pragma unroll
+      for (int n = 0; n < NS; ++n) colsum[g][n] = 0.f;
+    bool bad = false;
+    if (!all_exact) {
+      if (s_begin < s_end) {
+        issue(s_begin, sq0);
+        commit(sl0);
+        __syncthreads();
+        for (int s = s_begin; s < s_end; s += 2) {
+          step(s, sq0, sl0, sq1, sl1);
+          if (s + 1 < s_end) step(s + 1, sq1, sl1, sq0, sl0);
+        }
       }
+      // Each half-wave sum at most 2^63 keeps the column's sum within 2^64.
+#pragma unroll
+      for (int g = 0; g < GC; ++g)
+#pragma unroll
+        for (int n = 0; n < NS; ++n) bad |= !masked[n] && !(colsum[g][n] <= 0.5f * kOverflow);
     }
 
-    // Combine the half-wave sums and write this chunk's columns.
+    // Block-wide: a large bias, or a column sum out of the safe range, takes the
+    // chunk through the exact sweep.
+    if (all_exact || __syncthreads_or(bad)) {
+      auto xstep = [&](int s, const uint16_t* sq, const float* sl, uint16_t* nsq, float* nsl)
+                       __attribute__((always_inline)) {
+        const bool more = s + 1 < s_end;
+        if (more) issue(s + 1, nsq);
+        const int i0 = (qt_hi - s) * 32;
+        const int dmin = i0 - (jw + WK - 1);
+        const int dmax = i0 + 31 - jw;
+        if (!(dmax < window || dmin > hz)) exact_step(sq, sl, i0);
+        if (more) commit(nsl);
+        __syncthreads();
+      };
 #pragma unroll
-    for (int g = 0; g < GC; ++g) {
+      for (int g = 0; g < GC; ++g)
 #pragma unroll
-      for (int n = 0; n < NS; ++n) {
-        float v = colsum[g][n] + __shfl_xor(colsum[g][n], 32);
-        if (HAS_BIAS) v *= fac[n];
-        const int j = jw + 32 * n + l32;
-        if (hi == 0 && j < T && (!EPI || out)) {
-          if (!EPI && split) atomicAdd(&out[(head0 + g) * T + j], v);
-          else out[(head0 + g) * T + j] = v;
+        for (int n = 0; n < NS; ++n) {
+          colsum[g][n] = 0.f;
+          mref[g][n] = -__builtin_inff();
         }
-        if (EPI) aggv[n] = agg_mean ? aggv[n] + v : fmaxf(aggv[n], v);
+      if (s_begin < s_end) {
+        issue(s_begin, sq0);
+        commit(sl0);
+        __syncthreads();
+        for (int s = s_begin; s < s_end; s += 2) {
+          xstep(s, sq0, sl0, sq1, sl1);
+          if (s + 1 < s_end) xstep(s + 1, sq1, sl1, sq0, sl0);
+        }
+      }
+      // Combine the half-wave (mref, sum) pairs and write exp2(m + log2 sum).
+#pragma unroll
+      for (int g = 0; g < GC; ++g) {
+#pragma unroll
+        for (int n = 0; n < NS; ++n) {
+          const float mo = __shfl_xor(mref[g][n], 32);
+          const float so = __shfl_xor(colsum[g][n], 32);
+          const float mm = fmaxf(mref[g][n], mo);
+          float v = 0.f;
+          if (mm == __builtin_inff()) {
+            v = mm;
+          } else if (mm > -__builtin_inff()) {
+            const float tot = colsum[g][n] * exp2_fast(mref[g][n] - mm) + so * exp2_fast(mo - mm);
+            v = exp2_fast(mm + __log2f(tot));
+          }
+          if (masked[n]) v = 0.f;
+          const int j = jw + 32 * n + l32;
+          if (hi == 0 && j < T && (!EPI || out)) {
+            if (!EPI && split) atomicAdd(&out[(head0 + g) * T + j], v);
+            else out[(head0 + g) * T + j] = v;
+          }
+          if (EPI) aggv[n] = agg_mean ? aggv[n] + v : fmaxf(aggv[n], v);
+        }
+      }
+    } else {
+      // Combine the half-wave sums and write this chunk's columns.
+#pragma unroll
+      for (int g = 0; g < GC; ++g) {
+#pragma unroll
+        for (int n = 0; n < NS; ++n) {
+          float v = colsum[g][n] + __shfl_xor(colsum[g][n], 32);
+          if (HAS_BIAS) v = masked[n] ? 0.f : v * fac[n];
+          const int j = jw + 32 * n + l32;
+          if (hi == 0 && j < T && (!EPI || out)) {
+            if (!EPI && split) atomicAdd(&out[(head0 + g) * T + j], v);
+            else out[(head0 + g) * T + j] = v;
+          }
+          if (EPI) aggv[n] = agg_mean ? aggv[n] + v : fmaxf(aggv[n], v);
+        }
       }
     }
   }
@@ -738,8 +885,13 @@ int launch_p1_d(const Launch& L) {
   return launch_p1_b<D, 1>(L);
 }
 
+// Pass-2 launch forms for grids under kP2SmallGrid workgroups (8 per CU), where
+// the heaviest key blocks would set the time alone.
+constexpr long long kP2SmallGrid = 2048;
+constexpr int kP2SmallMode = 1;  // 0: whole sweeps; 1: sweeps split in two halves; 2: heads split
+
 template <int D, int NS, int GC, bool HB, bool EPI>
-int launch_p2(const Launch& L) {
+int launch_p2(const Launch& L, int hs) {
   constexpr int BK = 4 * NS * 32;
   const int nkb = (L.T + BK - 1) / BK;
   const long long grid = (long long)nkb * L.B * L.Hkv;
@@ -754,10 +906,9 @@ int launch_p2(const Launch& L) {
     const int ng = nbh / 8;
     xgroups = ng % 2 == 0 && (long long)ng * nkb >= 4 * 64 ? ng / 2 : ng;
   }
-  // Under 2048 workgroups (8 per CU) the heaviest key blocks set the time: split
-  // every block's sweep in two, into a zero-filled output (not with the epilogue,
-  // which needs each key's whole mass).
-  const int split = !EPI && grid < 2048;
+  // Split every block's sweep in two, into a zero-filled output (not with the
+  // epilogue, which needs each key's whole mass).
+  const int split = !EPI && hs == 1 && kP2SmallMode == 1 && grid < kP2SmallGrid;
   if (split) {
     const long long n = (long long)L.B * L.Hq * L.T;
     const long long fg = (n + 255) / 256;
@@ -766,26 +917,32 @@ int launch_p2(const Launch& L) {
     const int e = (int)hipGetLastError();
     if (e) return e;
   }
-  hipLaunchKernelGGL((future_mass_kernel<D, NS, GC, HB, EPI>), dim3((unsigned)(split ? 2 * grid : grid)), dim3(256),
-                     0, (hipStream_t)L.stream, reinterpret_cast<const uint16_t*>(L.q),
+  const long long nwg = split ? 2 * grid : grid * hs;
+  hipLaunchKernelGGL((future_mass_kernel<D, NS, GC, HB, EPI>), dim3((unsigned)nwg), dim3(256), 0,
+                     (hipStream_t)L.stream, reinterpret_cast<const uint16_t*>(L.q),
                      reinterpret_cast<const uint16_t*>(L.k), L.bias, L.lse, L.out, L.B, L.Hq, L.Hkv, L.T, c, L.window,
-                     hz, L.scores, L.agg, L.eps, L.normalize, split ? 0 : xgroups, split);
+                     hz, L.scores, L.agg, L.eps, L.normalize, (split || hs > 1) ? 0 : xgroups, split, hs);
   return (int)hipGetLastError();
 }
 
 template <int D, int NS, int GC>
-int launch_p2_b(const Launch& L) {
-  if (L.scores) return L.bias ? launch_p2<D, NS, GC, true, true>(L) : launch_p2<D, NS, GC, false, true>(L);
-  return L.bias ? launch_p2<D, NS, GC, true, false>(L) : launch_p2<D, NS, GC, false, false>(L);
+int launch_p2_b(const Launch& L, int hs) {
+  if (L.scores) return L.bias ? launch_p2<D, NS, GC, true, true>(L, 1) : launch_p2<D, NS, GC, false, true>(L, 1);
+  return L.bias ? launch_p2<D, NS, GC, true, false>(L, hs) : launch_p2<D, NS, GC, false, false>(L, hs);
 }
 
 template <int D, int NS>
 int launch_p2_gc(const Launch& L) {
-  // Query heads per step: the largest of 4, 2, 1 that divides G.
   const int G = L.Hq / L.Hkv;
-  if (G % 4 == 0) return launch_p2_b<D, NS, 4>(L);
-  if (G % 2 == 0) return launch_p2_b<D, NS, 2>(L);
-  return launch_p2_b<D, NS, 1>(L);
+  constexpr int BK = 4 * NS * 32;
+  const long long grid = (long long)((L.T + BK - 1) / BK) * L.B * L.Hkv;
+  // A small grid without the epilogue: heads split over more workgroups, two query
+  // heads per step.
+  if (kP2SmallMode == 2 && !L.scores && grid < kP2SmallGrid && G % 2 == 0) return launch_p2_b<D, NS, 2>(L, G / 2);
+  // Query heads per step: the largest of 4, 2, 1 that divides G.
+  if (G % 4 == 0) return launch_p2_b<D, NS, 4>(L, 1);
+  if (G % 2 == 0) return launch_p2_b<D, NS, 2>(L, 1);
+  return launch_p2_b<D, NS, 1>(L, 1);
 }
 
 template <int D>

@@ -216,3 +216,34 @@ def test_sparse_attn_argument_checks():
     assert _sa(d, lse=C_ + 16) == EINVAL                 # lse over v
     assert _sa(d, o=D_ - 16) == EINVAL                   # o over evict
     assert _sa(d, lse=E_ + 32) == EINVAL                 # lse over o
+
+
+def test_forced_hip_error_path(monkeypatch):
+    """The KVPOP_EHIP path, forced from the host (no GPU, nothing launched): with
+    KVPOP_TEST_FORCE_EHIP set to a HIP error code, every entry point that passes
+    validation returns KVPOP_EHIP, and kvpop_strerror(KVPOP_EHIP) returns that
+    error's text on the calling thread only."""
+    import threading
+    code = 719  # hipErrorLaunchFailure
+    monkeypatch.setenv("KVPOP_TEST_FORCE_EHIP", str(code))
+    d = _dims()
+    calls = [lambda: _lse(d), lambda: _p2(d), lambda: _tgt(d), lambda: _sc(d), lambda: _tk(),
+             lambda: _sa(d)]
+    for c in calls:
+        assert c() == kv.KVPOP_EHIP
+        text = kv.kvpop_strerror(kv.KVPOP_EHIP)
+        assert text.startswith("HIP error: ") and len(text) > len("HIP error: ")
+    # validation still comes first
+    assert _lse(_dims(B=0)) == EINVAL
+    assert _sa(d, q=None) == EINVAL
+    # the text is per thread: a thread that has not failed sees the generic text
+    seen = []
+    th = threading.Thread(target=lambda: seen.append(kv.kvpop_strerror(kv.KVPOP_EHIP)))
+    th.start()
+    th.join()
+    assert seen == ["HIP runtime error"]
+    # the binding's exception carries the status and this thread's text
+    err = kv.KvpopError(_lse(d), "kvpop_row_lse")
+    assert err.status == kv.KVPOP_EHIP and "HIP error: " in str(err)
+    monkeypatch.delenv("KVPOP_TEST_FORCE_EHIP")
+    assert _lse(_dims(B=0)) == EINVAL

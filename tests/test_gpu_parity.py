@@ -6,6 +6,7 @@ within 5e-4 absolute. Inputs are the same bf16 bit patterns on both sides, from
 the seeded generator in ``workload``.
 """
 import math
+import os
 
 import numpy as np
 import pytest
@@ -20,6 +21,7 @@ pytestmark = pytest.mark.gpu
 
 REL = 2e-3
 LSE_ABS = 5e-4
+THREADS = max(1, min(16, len(os.sched_getaffinity(0))))  # host threads for the blocked oracle
 
 
 def _dev(bits: np.ndarray):
@@ -215,6 +217,19 @@ def test_qwen3_4b_w1024_full_size_sampled():
                                    rtol=0)
 
 
+def test_qwen3_4b_w1024_full_size_one_head_exhaustive():
+    """Full T=16384, B=2 W=1024 workload with the sink: every key and every LSE row
+    of one (b, query head) against the blocked oracle."""
+    w = workload.make("qwen3_4b_t16k_w1024")
+    out, lse = _run(w, 1, 1024)
+    b, qh = 1, 22
+    q, k = w.q_bits[b, qh], w.k_bits[b, qh // w.G]
+    lse_ref = oracle.row_lse_blocked(q, k, w.scale, w.bias, threads=THREADS)
+    _check_lse(lse[b, qh], lse_ref, "16k W=1024 b%d qh%d" % (b, qh))
+    ref = oracle.future_mass_blocked(q, k, w.scale, w.bias, 1, 1024, lse=lse_ref, threads=THREADS)
+    _check_out(out[b, qh], ref, 1, "16k W=1024 b%d qh%d" % (b, qh))
+
+
 def test_qwen3_8b_t32k_full_scale():
     """Qwen3-8B shape at T=32768, B=4, heavy hitters: the full workload on the GPU,
     every head by the row sum, sampled LSE rows and the last keys of several heads
@@ -286,6 +301,61 @@ def test_qwen3_8b_t32k_one_head_exhaustive():
 def _harmonic(n):
     # H_n in fp64 by direct summation in reverse (small to large)
     return np.concatenate([[0.0], np.cumsum(1.0 / np.arange(1, n + 1))])
+
+
+@pytest.mark.timeout(900)
+def test_long_t128k_as_generated():
+    """The T=131072 workload exactly as generated (B=1, 32 query heads on 8 KV heads,
+    drifting clusters) in the benchmark's launch sequence: pass 1 once, then pass 2
+    for the bands (0, -1) and (1, 4096) from that one LSE. With B * Hkv = 8 every
+    XCD runs one (b, KV head) group in an unsplit launch. Checked: the full-band
+    masses of every head sum to T; sampled LSE rows of two query heads of every KV
+    head; every LSE row and every key of both bands for query head 5 (KV head 1);
+    every LSE row and every key of the W = 4096 band for query head 30 (KV head 7)."""
+    w = workload.make("long_t128k")
+    assert (w.B, w.Hq, w.Hkv, w.T, w.D) == (1, 32, 8, 131072, 128) and w.bands == [(0, -1), (1, 4096)]
+    q, k = _dev(w.q_bits), _dev(w.k_bits)
+    lse_d = kv.kvpop_row_lse(q, k, w.scale)
+    outs_d = [kv.kvpop_future_attn_from_lse(q, k, lse_d, w.scale, a, h) for a, h in w.bands]
+    torch.cuda.synchronize()
+    lse = lse_d.cpu().numpy().astype(np.float64)
+    full, wband = [o.cpu().numpy().astype(np.float64) for o in outs_d]
+    del q, k, lse_d, outs_d
+    np.testing.assert_allclose(full.sum(axis=-1), w.T, rtol=REL)
+    rng = np.random.default_rng(5)
+    for h in range(w.Hkv):
+        for qh in (h * w.G, h * w.G + 3):
+            rows = sorted(set(rng.integers(0, w.T, 4).tolist()) | {0, 8191, 8192, w.T - 1})
+            np.testing.assert_allclose(lse[0, qh, rows], oracle.row_lse_rows(w.q_bits[0, qh], w.k_bits[0, h], w.scale,
+                                                                             rows), atol=LSE_ABS, rtol=0)
+    for qh, bands in [(5, [0, 1]), (30, [1])]:
+        qv, kv_ = w.q_bits[0, qh], w.k_bits[0, qh // w.G]
+        lse_ref = oracle.row_lse_blocked(qv, kv_, w.scale, block=512, threads=THREADS)
+        _check_lse(lse[0, qh], lse_ref, "128k qh%d" % qh)
+        for i in bands:
+            a, h = w.bands[i]
+            ref = oracle.future_mass_blocked(qv, kv_, w.scale, None, a, h, lse=lse_ref, block=512, threads=THREADS)
+            _check_out((full, wband)[i][0, qh], ref, a, "128k qh%d band %s" % (qh, (a, h)))
+
+
+def test_long_constant_keys_harmonic():
+    """Every key equal (k_t = k) with the workload's random queries: each row is
+    uniform whatever Q is, so LSE_d = scale <q_d, k> + log(d + 1) and the masses are
+    the harmonic forms of Q = 0, at T = 131072 on real MFMA tiles."""
+    T = 131072
+    w = workload.make("long_t128k", Hq=4, Hkv=1)
+    w.k_bits[:] = w.k_bits[:, :, 777:778, :]
+    H = _harmonic(T + 1)
+    t = np.arange(T)
+    out, lse = _run(w, 0, -1)
+    kk = oracle.bf16_bits_to_f64(w.k_bits[0, 0, 0])
+    for qh in range(4):
+        a = w.scale * (oracle.bf16_bits_to_f64(w.q_bits[0, qh]) @ kk)
+        np.testing.assert_allclose(lse[0, qh], a + np.log(t + 1.0), atol=LSE_ABS, rtol=0)
+    _check_out(out, np.broadcast_to(H[T] - H[t], out.shape), 0, "constant keys full")
+    out, _ = _run(w, 1, 4096)
+    ref = np.where(t + 1 <= T - 1, H[np.minimum(T, t + 4097)] - H[np.minimum(t + 1, T)], 0.0)
+    _check_out(out, np.broadcast_to(ref, out.shape), 1, "constant keys W=4096")
 
 
 def test_long_q_zero_harmonic():

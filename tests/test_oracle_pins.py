@@ -316,6 +316,11 @@ def test_transposed_blocked_columns_agree(w, h):
                                rtol=1e-12, atol=1e-300)
     lse_b = oracle.row_lse_blocked(Q[0, 0], K[0, 0], 0.35, bias, block=50)
     np.testing.assert_allclose(lse_b, oracle.row_lse(Q, K, 0.35, bias)[0, 0], rtol=1e-13, atol=1e-14)
+    # the same blocks on several host threads
+    np.testing.assert_allclose(oracle.row_lse_blocked(Q[0, 0], K[0, 0], 0.35, bias, block=50, threads=3), lse_b,
+                               rtol=1e-13, atol=1e-14)
+    np.testing.assert_allclose(oracle.future_mass_blocked(Q[0, 0], K[0, 0], 0.35, bias, w, h, block=32, threads=4),
+                               ref, rtol=1e-12, atol=1e-300)
     np.testing.assert_allclose(oracle.row_lse_rows(Q[0, 0], K[0, 0], 0.35, [0, 7, 202], bias), lse_b[[0, 7, 202]],
                                rtol=1e-13, atol=1e-14)
 
