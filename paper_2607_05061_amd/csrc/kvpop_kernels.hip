@@ -393,8 +393,9 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
 // its 16 query rows of each tile into a per-tile sum and then into a running
 // column sum (a two-level sum keeps the fp32 error near (16 + tiles) ulp). At the
 // end the two half-wave sums of each column are added and written: each workgroup
-// owns its output columns, so results are deterministic. (A split launch, for
-// small grids, adds exactly two partial sums per column into a zeroed output.)
+// owns its output columns, so results are deterministic, with no atomics. (A
+// small grid splits the query heads of a key block over several workgroups; each
+// still owns its (head, key) outputs and sums them in the same order.)
 //
 // Query rows beyond T get LSE = +inf in LDS, which zeroes their terms. A per-key
 // bias is factored out of the sum, out_t = exp(bias_t) * sum_d exp(...). Query
@@ -424,7 +425,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_pe
 future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const float* __restrict__ bias,
                    const float* __restrict__ lse, float* __restrict__ out, int B, int Hq, int Hkv, int T, float c,
                    int window, int hz, float* __restrict__ scores, int agg_mean, float eps, int normalize,
-                   int xgroups, int split, int hs) {
+                   int xgroups, int hs) {
   using TL = Tile<D>;
   constexpr int KS = TL::KS;
   constexpr int WK = NS * 32;  // keys per wave
@@ -446,19 +447,11 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
   // of groups heaviest key block first: more workgroups of one group then sweep
   // the same query tiles together and share them in that XCD's L2. Otherwise the
   // order is key block major, heaviest first, over all groups.
-  // A split launch (a small grid, no epilogue) gives each half of a key block's
-  // sweep its own workgroup, heaviest block first; the two halves add their partial
-  // sums into the zero-filled output, and a + b = b + a keeps the result exact to
-  // the bit whichever lands first.
-  int kb, bh, half = 0, ch = 0;
-  if (split) {
-    const int u = blockIdx.x / nbh;
-    kb = u >> 1;
-    half = u & 1;
-    bh = blockIdx.x - u * nbh;
-  } else if (hs > 1) {
-    // Head-split launch: hs workgroups per (key block, group), workgroup ch taking
-    // the head chunks ch, ch + hs, ...; key block major, heaviest first.
+  // A head-split launch (a small grid, no epilogue) gives each (key block, group)
+  // hs workgroups, workgroup ch taking the head chunks ch, ch + hs, ...; key block
+  // major, heaviest first. Every workgroup still owns its output columns.
+  int kb, bh, ch = 0;
+  if (hs > 1) {
     const int per = nbh * hs;
     kb = blockIdx.x / per;
     const int r = blockIdx.x - kb * per;
@@ -488,9 +481,6 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     qt_hi = (int)(r_hi / 32);
     nqt = qt_hi - (int)(r_lo / 32) + 1;
   }
-  // The steps of the sweep this workgroup takes (its half in a split launch).
-  const int s_begin = split && half ? nqt / 2 : 0;
-  const int s_end = split && !half ? nqt / 2 : nqt;
 
   // Bias of this lane's key columns: factored out (fac) by the fast sweep, added to
   // every exponent (bl2, log2 units) by the exact sweep. masked: bias -inf.
@@ -740,7 +730,7 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     };
 
     auto step = [&](int s, const uint16_t* sq, const float* sl, uint16_t* nsq, float* nsl) __attribute__((always_inline)) {
-      const bool more = s + 1 < s_end;
+      const bool more = s + 1 < nqt;
       if (more) issue(s + 1, nsq);
       const int i0 = (qt_hi - s) * 32;
       // Differences d = i - j over this wave's keys and the tile's rows.
@@ -761,13 +751,13 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
       for (int n = 0; n < NS; ++n) colsum[g][n] = 0.f;
     bool bad = false;
     if (!all_exact) {
-      if (s_begin < s_end) {
-        issue(s_begin, sq0);
+      if (nqt > 0) {
+        issue(0, sq0);
         commit(sl0);
         __syncthreads();
-        for (int s = s_begin; s < s_end; s += 2) {
+        for (int s = 0; s < nqt; s += 2) {
           step(s, sq0, sl0, sq1, sl1);
-          if (s + 1 < s_end) step(s + 1, sq1, sl1, sq0, sl0);
+          if (s + 1 < nqt) step(s + 1, sq1, sl1, sq0, sl0);
         }
       }
       // Each half-wave sum at most 2^63 keeps the column's sum within 2^64.
@@ -782,7 +772,7 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     if (all_exact || __syncthreads_or(bad)) {
       auto xstep = [&](int s, const uint16_t* sq, const float* sl, uint16_t* nsq, float* nsl)
                        __attribute__((always_inline)) {
-        const bool more = s + 1 < s_end;
+        const bool more = s + 1 < nqt;
         if (more) issue(s + 1, nsq);
         const int i0 = (qt_hi - s) * 32;
         const int dmin = i0 - (jw + WK - 1);
@@ -798,13 +788,13 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
           colsum[g][n] = 0.f;
           mref[g][n] = -__builtin_inff();
         }
-      if (s_begin < s_end) {
-        issue(s_begin, sq0);
+      if (nqt > 0) {
+        issue(0, sq0);
         commit(sl0);
         __syncthreads();
-        for (int s = s_begin; s < s_end; s += 2) {
+        for (int s = 0; s < nqt; s += 2) {
           xstep(s, sq0, sl0, sq1, sl1);
-          if (s + 1 < s_end) xstep(s + 1, sq1, sl1, sq0, sl0);
+          if (s + 1 < nqt) xstep(s + 1, sq1, sl1, sq0, sl0);
         }
       }
       // Combine the half-wave (mref, sum) pairs and write exp2(m + log2 sum).
@@ -825,8 +815,7 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
           if (masked[n]) v = 0.f;
           const int j = jw + 32 * n + l32;
           if (hi == 0 && j < T && (!EPI || out)) {
-            if (!EPI && split) atomicAdd(&out[(head0 + g) * T + j], v);
-            else out[(head0 + g) * T + j] = v;
+            out[(head0 + g) * T + j] = v;
           }
           if (EPI) aggv[n] = agg_mean ? aggv[n] + v : fmaxf(aggv[n], v);
         }
@@ -841,8 +830,7 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
           if (HAS_BIAS) v = masked[n] ? 0.f : v * fac[n];
           const int j = jw + 32 * n + l32;
           if (hi == 0 && j < T && (!EPI || out)) {
-            if (!EPI && split) atomicAdd(&out[(head0 + g) * T + j], v);
-            else out[(head0 + g) * T + j] = v;
+            out[(head0 + g) * T + j] = v;
           }
           if (EPI) aggv[n] = agg_mean ? aggv[n] + v : fmaxf(aggv[n], v);
         }
@@ -850,11 +838,6 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     }
   }
   if (EPI) write_scores();
-}
-
-// Zeroes n floats (the output of a split pass-2 launch).
-__global__ __launch_bounds__(256) void zero_fill_kernel(float* __restrict__ p, long long n) {
-  for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < n; i += (long long)gridDim.x * 256) p[i] = 0.f;
 }
 
 template <int D, int P, bool HB>
@@ -885,11 +868,6 @@ int launch_p1_d(const Launch& L) {
   return launch_p1_b<D, 1>(L);
 }
 
-// Pass-2 launch forms for grids under kP2SmallGrid workgroups (8 per CU), where
-// the heaviest key blocks would set the time alone.
-constexpr long long kP2SmallGrid = 2048;
-constexpr int kP2SmallMode = 1;  // 0: whole sweeps; 1: sweeps split in two halves; 2: heads split
-
 template <int D, int NS, int GC, bool HB, bool EPI>
 int launch_p2(const Launch& L, int hs) {
   constexpr int BK = 4 * NS * 32;
@@ -906,22 +884,10 @@ int launch_p2(const Launch& L, int hs) {
     const int ng = nbh / 8;
     xgroups = ng % 2 == 0 && (long long)ng * nkb >= 4 * 64 ? ng / 2 : ng;
   }
-  // Split every block's sweep in two, into a zero-filled output (not with the
-  // epilogue, which needs each key's whole mass).
-  const int split = !EPI && hs == 1 && kP2SmallMode == 1 && grid < kP2SmallGrid;
-  if (split) {
-    const long long n = (long long)L.B * L.Hq * L.T;
-    const long long fg = (n + 255) / 256;
-    hipLaunchKernelGGL(zero_fill_kernel, dim3((unsigned)(fg < 4096 ? fg : 4096)), dim3(256), 0,
-                       (hipStream_t)L.stream, L.out, n);
-    const int e = (int)hipGetLastError();
-    if (e) return e;
-  }
-  const long long nwg = split ? 2 * grid : grid * hs;
-  hipLaunchKernelGGL((future_mass_kernel<D, NS, GC, HB, EPI>), dim3((unsigned)nwg), dim3(256), 0,
+  hipLaunchKernelGGL((future_mass_kernel<D, NS, GC, HB, EPI>), dim3((unsigned)(grid * hs)), dim3(256), 0,
                      (hipStream_t)L.stream, reinterpret_cast<const uint16_t*>(L.q),
                      reinterpret_cast<const uint16_t*>(L.k), L.bias, L.lse, L.out, L.B, L.Hq, L.Hkv, L.T, c, L.window,
-                     hz, L.scores, L.agg, L.eps, L.normalize, (split || hs > 1) ? 0 : xgroups, split, hs);
+                     hz, L.scores, L.agg, L.eps, L.normalize, hs > 1 ? 0 : xgroups, hs);
   return (int)hipGetLastError();
 }
 
@@ -936,9 +902,17 @@ int launch_p2_gc(const Launch& L) {
   const int G = L.Hq / L.Hkv;
   constexpr int BK = 4 * NS * 32;
   const long long grid = (long long)((L.T + BK - 1) / BK) * L.B * L.Hkv;
-  // A small grid without the epilogue: heads split over more workgroups, two query
-  // heads per step.
-  if (kP2SmallMode == 2 && !L.scores && grid < kP2SmallGrid && G % 2 == 0) return launch_p2_b<D, NS, 2>(L, G / 2);
+  // Under 2048 workgroups (8 per CU) with a long band the heaviest key blocks set
+  // the time: the query heads of each (key block, group) are then split over
+  // several workgroups (not with the epilogue, which aggregates all G heads of a
+  // key in one workgroup). Under 512 workgroups each takes one head, else two.
+  // With a short band every block does about the same work and splitting does
+  // not pay.
+  const bool long_band = L.horizon < 0 || L.horizon >= L.T / 2;
+  if (!L.scores && grid < 2048 && long_band && G > 1) {
+    if (grid >= 512 && G % 2 == 0) return launch_p2_b<D, NS, 2>(L, G / 2);
+    return launch_p2_b<D, NS, 1>(L, G);
+  }
   // Query heads per step: the largest of 4, 2, 1 that divides G.
   if (G % 4 == 0) return launch_p2_b<D, NS, 4>(L, 1);
   if (G % 2 == 0) return launch_p2_b<D, NS, 2>(L, 1);
