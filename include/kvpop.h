@@ -62,7 +62,7 @@
 extern "C" {
 #endif
 
-#define KVPOP_ABI_VERSION 2
+#define KVPOP_ABI_VERSION 3
 
 /* Status codes returned by every entry point. */
 enum {
@@ -73,8 +73,10 @@ enum {
                              buffers, or a size whose element count overflows int64 */
   KVPOP_EUNSUPPORTED = 2, /* head_dim not in {64, 128}, a base pointer not 16-byte
                              aligned, or T above KVPOP_MAX_SEQ_LEN */
-  KVPOP_EHIP = 3          /* the HIP runtime reported an error while launching;
+  KVPOP_EHIP = 3,         /* the HIP runtime reported an error while launching;
                              kvpop_strerror(KVPOP_EHIP) then returns its text */
+  KVPOP_ETOOBIG = 4       /* kvpop_running_topk_noalloc: the problem's workspace exceeds
+                             KVPOP_NOALLOC_SCRATCH_BYTES */
 };
 
 #define KVPOP_MAX_SEQ_LEN (1 << 24)
@@ -189,6 +191,26 @@ size_t kvpop_running_topk_workspace_size(const kvpop_topk_dims* dims);
 int kvpop_running_topk(const kvpop_topk_dims* dims, const float* scores, const float* log_gamma, int32_t sinks,
                        int32_t window, int32_t topk, int32_t* rank, int32_t* cutoff, int32_t* label,
                        int32_t* boundary, int32_t* evict, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of device scratch that kvpop_running_topk_noalloc holds per GPU (32 MiB:
+ * every (B, H, T) with kvpop_running_topk_workspace_size up to this, e.g. B*H = 32
+ * sequences of T = 32768 or B*H = 8 of T = 131072). */
+#define KVPOP_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): kvpop_running_topk with
+ * the same arguments and outputs but no workspace argument. Its workspace is a
+ * device array of KVPOP_NOALLOC_SCRATCH_BYTES inside the library, one per GPU,
+ * held from the first call on that GPU until the process ends; the call allocates
+ * nothing. A problem whose kvpop_running_topk_workspace_size exceeds that is
+ * rejected with KVPOP_ETOOBIG before anything is launched. All calls on one GPU
+ * share its array, whose contents on entry do not matter: calls that overlap on
+ * one GPU (unordered streams, or host threads without ordering) race and give
+ * wrong results; calls ordered on one stream are safe. The first call on a GPU
+ * looks up the array's device address (KVPOP_EHIP if that fails). */
+int kvpop_running_topk_noalloc(const kvpop_topk_dims* dims, const float* scores, const float* log_gamma,
+                               int32_t sinks, int32_t window, int32_t topk, int32_t* rank, int32_t* cutoff,
+                               int32_t* label, int32_t* boundary, int32_t* evict, void* stream);
 
 /* Human-readable text for a status code. For KVPOP_EHIP it is the HIP runtime's
  * message for the last failure on the calling thread. Never returns NULL; the

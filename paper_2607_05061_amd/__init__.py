@@ -25,15 +25,18 @@ __all__ = [
     "lib", "lib_path", "kvpop_row_lse", "kvpop_future_attn_from_lse", "kvpop_future_attn_target",
     "kvpop_future_attn_scores", "kvpop_strerror", "kvpop_abi_version", "KVPOP_AGG_MAX", "KVPOP_AGG_MEAN",
     "KvpopTopkDims", "kvpop_running_topk", "kvpop_running_topk_workspace_size", "kvpop_sparse_attn_fwd",
+    "kvpop_running_topk_noalloc", "KVPOP_ETOOBIG", "KVPOP_NOALLOC_SCRATCH_BYTES",
 ]
 
 KVPOP_OK = 0
 KVPOP_EINVAL = 1
 KVPOP_EUNSUPPORTED = 2
 KVPOP_EHIP = 3
+KVPOP_ETOOBIG = 4
+KVPOP_NOALLOC_SCRATCH_BYTES = 32 << 20
 KVPOP_AGG_MAX = 0
 KVPOP_AGG_MEAN = 1
-ABI_VERSION = 2
+ABI_VERSION = 3
 
 _PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 _LIB: Optional[ctypes.CDLL] = None
@@ -90,6 +93,9 @@ def lib() -> ctypes.CDLL:
         L.kvpop_running_topk.argtypes = [ctypes.POINTER(KvpopTopkDims), P, P, I32, I32, I32, P, P, P, P, P, P,
                                          ctypes.c_size_t, P]
         L.kvpop_running_topk.restype = ctypes.c_int
+        L.kvpop_running_topk_noalloc.argtypes = [ctypes.POINTER(KvpopTopkDims), P, P, I32, I32, I32, P, P, P, P, P,
+                                                 P]
+        L.kvpop_running_topk_noalloc.restype = ctypes.c_int
         L.kvpop_sparse_attn_fwd.argtypes = [ctypes.POINTER(KvpopDims), P, P, P, P, P, P, P, P]
         L.kvpop_sparse_attn_fwd.restype = ctypes.c_int
         L.kvpop_strerror.argtypes = [ctypes.c_int]
@@ -279,6 +285,43 @@ def kvpop_running_topk(scores, sinks: int, window: int, topk: int, log_gamma=Non
     if st != KVPOP_OK:
         raise KvpopError(st, "kvpop_running_topk")
     return out
+
+
+def kvpop_running_topk_noalloc(scores, sinks: int, window: int, topk: int, log_gamma=None, labels: bool = True,
+                               evict: bool = False, out=None, stream=None):
+    """kvpop_running_topk without a workspace: the library's own per-GPU scratch array
+    serves instead (see include/kvpop.h). ``out`` may hold preallocated int32 [B, H, T]
+    outputs ("rank", "cutoff" and, as requested, "label", "boundary", "evict"), so that
+    the call itself allocates nothing; missing ones are allocated here."""
+    torch = _torch()
+    _check_tensor(scores, "scores", torch.float32, None)
+    if scores.dim() != 3:
+        raise ValueError("scores must be [B, H, T]")
+    B, H, T = scores.shape
+    if log_gamma is not None:
+        _check_tensor(log_gamma, "log_gamma", torch.float32, scores.device)
+        if tuple(log_gamma.shape) != (H,):
+            raise ValueError("log_gamma must be [H]")
+    names = ["rank", "cutoff"] + (["label", "boundary"] if labels else []) + (["evict"] if evict else [])
+    res = {}
+    for n in names:
+        x = (out or {}).get(n)
+        if x is None:
+            x = torch.empty((B, H, T), dtype=torch.int32, device=scores.device)
+        else:
+            _check_tensor(x, n, torch.int32, scores.device)
+            if tuple(x.shape) != (B, H, T):
+                raise ValueError("%s must be [B, H, T]" % n)
+        res[n] = x
+    d = KvpopTopkDims(B, H, T)
+    ptr = lambda n: res[n].data_ptr() if n in res else None  # noqa: E731
+    st = lib().kvpop_running_topk_noalloc(ctypes.byref(d), scores.data_ptr(),
+                                          log_gamma.data_ptr() if log_gamma is not None else None, int(sinks),
+                                          int(window), int(topk), ptr("rank"), ptr("cutoff"), ptr("label"),
+                                          ptr("boundary"), ptr("evict"), _stream_ptr(stream, scores.device))
+    if st != KVPOP_OK:
+        raise KvpopError(st, "kvpop_running_topk_noalloc")
+    return res
 
 
 def kvpop_sparse_attn_fwd(q, k, v, evict, scale: float, key_bias=None, o=None, lse=None, stream=None):

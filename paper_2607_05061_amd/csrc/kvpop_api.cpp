@@ -118,6 +118,55 @@ int check_output(const void* out, int64_t bytes, const Sizes& sz, const kvpop_di
   return KVPOP_OK;
 }
 
+// Validation shared by kvpop_running_topk and kvpop_running_topk_noalloc. The
+// workspace (need bytes) is checked only when it is caller memory (ws != NULL).
+int check_topk(const kvpop_topk_dims* d, const float* scores, const float* log_gamma, int32_t sinks, int32_t window,
+               int32_t topk, int32_t* rank, int32_t* cutoff, int32_t* label, int32_t* boundary, int32_t* evict,
+               const void* ws, size_t need) {
+  if (!scores || !rank || !cutoff) return KVPOP_EINVAL;
+  const void* ptrs[] = {scores, log_gamma, rank, cutoff, label, boundary, evict, ws};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return KVPOP_EUNSUPPORTED;
+  const int64_t n = (int64_t)d->batch * d->n_heads * d->seq_len;
+  if (n / d->seq_len / d->n_heads != d->batch || n * 4 > INT64_MAX / 2) return KVPOP_EINVAL;
+  const int64_t b = n * 4;
+  // Outputs must not overlap each other, the inputs or the workspace.
+  const void* outs[] = {rank, cutoff, label, boundary, evict};
+  for (int i = 0; i < 5; ++i) {
+    if (!outs[i]) continue;
+    if (overlap(outs[i], b, scores, b) || overlap(outs[i], b, log_gamma, (int64_t)d->n_heads * 4) ||
+        overlap(outs[i], b, ws, (int64_t)need))
+      return KVPOP_EINVAL;
+    for (int j = i + 1; j < 5; ++j)
+      if (overlap(outs[i], b, outs[j], b)) return KVPOP_EINVAL;
+  }
+  if (overlap(ws, (int64_t)need, scores, b) || overlap(ws, (int64_t)need, log_gamma, (int64_t)d->n_heads * 4))
+    return KVPOP_EINVAL;
+  return KVPOP_OK;
+}
+
+kvpop::TopkLaunch make_topk(const kvpop_topk_dims* d, const float* scores, const float* log_gamma, int32_t sinks,
+                            int32_t window, int32_t topk, int32_t* rank, int32_t* cutoff, int32_t* label,
+                            int32_t* boundary, int32_t* evict, void* workspace, void* stream) {
+  kvpop::TopkLaunch L{};
+  L.scores = scores;
+  L.log_gamma = log_gamma;
+  L.B = d->batch;
+  L.H = d->n_heads;
+  L.T = d->seq_len;
+  L.sinks = sinks;
+  L.window = window;
+  L.topk = topk;
+  L.rank = rank;
+  L.cutoff = cutoff;
+  L.label = label;
+  L.boundary = boundary;
+  L.evict = evict;
+  L.workspace = workspace;
+  L.stream = stream;
+  return L;
+}
+
 }  // namespace
 
 extern "C" {
@@ -135,6 +184,9 @@ const char* kvpop_strerror(int status) {
       return "unsupported configuration (head_dim not 64/128, pointer not 16-byte aligned, or size limit)";
     case KVPOP_EHIP:
       return g_err_text.empty() ? "HIP runtime error" : g_err_text.c_str();
+    case KVPOP_ETOOBIG:
+      return "problem too large for the no-allocation entry point (its workspace exceeds "
+             "KVPOP_NOALLOC_SCRATCH_BYTES)";
     default:
       return "unknown status code";
   }
@@ -221,41 +273,34 @@ int kvpop_running_topk(const kvpop_topk_dims* d, const float* scores, const floa
   if (!scores || !rank || !cutoff || !workspace) return KVPOP_EINVAL;
   const size_t need = kvpop_running_topk_workspace_size(d);
   if (need == 0 || workspace_bytes < need) return KVPOP_EINVAL;
-  const void* ptrs[] = {scores, log_gamma, rank, cutoff, label, boundary, evict, workspace};
-  for (const void* p : ptrs)
-    if (p && !aligned16(p)) return KVPOP_EUNSUPPORTED;
-  const int64_t n = (int64_t)d->batch * d->n_heads * d->seq_len;
-  if (n / d->seq_len / d->n_heads != d->batch || n * 4 > INT64_MAX / 2) return KVPOP_EINVAL;
-  const int64_t b = n * 4;
-  // Outputs must not overlap each other, the inputs or the workspace.
-  const void* outs[] = {rank, cutoff, label, boundary, evict};
-  for (int i = 0; i < 5; ++i) {
-    if (!outs[i]) continue;
-    if (overlap(outs[i], b, scores, b) || overlap(outs[i], b, log_gamma, (int64_t)d->n_heads * 4) ||
-        overlap(outs[i], b, workspace, (int64_t)need))
-      return KVPOP_EINVAL;
-    for (int j = i + 1; j < 5; ++j)
-      if (overlap(outs[i], b, outs[j], b)) return KVPOP_EINVAL;
-  }
-  if (overlap(workspace, (int64_t)need, scores, b) || overlap(workspace, (int64_t)need, log_gamma, (int64_t)d->n_heads * 4))
-    return KVPOP_EINVAL;
-  kvpop::TopkLaunch L{};
-  L.scores = scores;
-  L.log_gamma = log_gamma;
-  L.B = d->batch;
-  L.H = d->n_heads;
-  L.T = d->seq_len;
-  L.sinks = sinks;
-  L.window = window;
-  L.topk = topk;
-  L.rank = rank;
-  L.cutoff = cutoff;
-  L.label = label;
-  L.boundary = boundary;
-  L.evict = evict;
-  L.workspace = workspace;
-  L.stream = stream;
+  const int st = check_topk(d, scores, log_gamma, sinks, window, topk, rank, cutoff, label, boundary, evict,
+                            workspace, need);
+  if (st != KVPOP_OK) return st;
+  kvpop::TopkLaunch L = make_topk(d, scores, log_gamma, sinks, window, topk, rank, cutoff, label, boundary, evict,
+                                  workspace, stream);
   return launch([&] { return kvpop::launch_running_topk(L); });
+}
+
+int kvpop_running_topk_noalloc(const kvpop_topk_dims* d, const float* scores, const float* log_gamma, int32_t sinks,
+                               int32_t window, int32_t topk, int32_t* rank, int32_t* cutoff, int32_t* label,
+                               int32_t* boundary, int32_t* evict, void* stream) {
+  if (!d || d->batch < 1 || d->n_heads < 1 || d->seq_len < 1) return KVPOP_EINVAL;
+  if (d->seq_len > KVPOP_MAX_SEQ_LEN) return KVPOP_EUNSUPPORTED;
+  if (sinks < 0 || window < 0 || topk < 1) return KVPOP_EINVAL;
+  const size_t need = kvpop_running_topk_workspace_size(d);
+  if (need == 0) return KVPOP_EINVAL;
+  if (need > (size_t)KVPOP_NOALLOC_SCRATCH_BYTES) return KVPOP_ETOOBIG;
+  const int st = check_topk(d, scores, log_gamma, sinks, window, topk, rank, cutoff, label, boundary, evict,
+                            nullptr, 0);
+  if (st != KVPOP_OK) return st;
+  return launch([&] {
+    void* ws = nullptr;
+    const int e = kvpop::noalloc_scratch(stream, &ws);
+    if (e != 0) return e;
+    kvpop::TopkLaunch L = make_topk(d, scores, log_gamma, sinks, window, topk, rank, cutoff, label, boundary,
+                                    evict, ws, stream);
+    return kvpop::launch_running_topk(L);
+  });
 }
 
 int kvpop_sparse_attn_fwd(const kvpop_dims* dims, const void* q, const void* k, const void* v,

@@ -23,6 +23,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
+#include "kvpop.h"
 #include "kvpop_internal.h"
 
 namespace kvpop {
@@ -451,6 +454,45 @@ size_t topk_workspace_words_per_seq(int T) {
   const int L = topk_levels(T);
   const size_t W1 = (size_t)(T + 31) / 32 + 1;
   return 6 * (size_t)T + 2 * (size_t)L * W1 + (size_t)L + 4;
+}
+
+// Scratch of kvpop_running_topk_noalloc: the workspace of the ranking kernels in a
+// file-scope device array instead of caller memory. Every GPU the library runs on
+// holds its own copy until the process ends; all calls on one GPU share it.
+static __device__ __align__(256) uint32_t scratch[KVPOP_NOALLOC_SCRATCH_BYTES / 4];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+// Device address of `scratch` on the device of `stream` (the current device for
+// the null stream), resolved once per device with that device current. In host
+// code the array's name is only a handle for the runtime, never an address.
+int noalloc_scratch(void* stream, void** ptr) {
+  int dev = 0;
+  hipError_t e = stream ? hipStreamGetDevice((hipStream_t)stream, &dev) : hipGetDevice(&dev);
+  if (e != hipSuccess) return (int)e;
+  if (dev < 0 || dev >= kMaxDevices) return (int)hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    int cur = 0;
+    e = hipGetDevice(&cur);
+    if (e != hipSuccess) return (int)e;
+    if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return (int)e;
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev) {
+      const hipError_t e2 = hipSetDevice(cur);
+      if (e == hipSuccess) e = e2;
+    }
+    if (e != hipSuccess) return (int)e;
+    if (!p) return (int)hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return 0;
 }
 
 int launch_running_topk(const TopkLaunch& L) {

@@ -26,7 +26,7 @@ def test_header_declares_the_entry_points():
     names = set(_declared_functions())
     assert names == {"kvpop_row_lse", "kvpop_future_attn_from_lse", "kvpop_future_attn_target",
                      "kvpop_future_attn_scores", "kvpop_running_topk", "kvpop_running_topk_workspace_size",
-                     "kvpop_sparse_attn_fwd", "kvpop_strerror", "kvpop_abi_version"}
+                     "kvpop_sparse_attn_fwd", "kvpop_strerror", "kvpop_abi_version", "kvpop_running_topk_noalloc"}
 
 
 def test_library_exports_every_declared_symbol():
@@ -37,14 +37,16 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version_and_strerror():
-    assert kv.kvpop_abi_version() == kv.ABI_VERSION == 2
-    texts = {c: kv.kvpop_strerror(c) for c in (kv.KVPOP_OK, kv.KVPOP_EINVAL, kv.KVPOP_EUNSUPPORTED, kv.KVPOP_EHIP, 99)}
+    assert kv.kvpop_abi_version() == kv.ABI_VERSION == 3
+    texts = {c: kv.kvpop_strerror(c) for c in (kv.KVPOP_OK, kv.KVPOP_EINVAL, kv.KVPOP_EUNSUPPORTED, kv.KVPOP_EHIP,
+                                               kv.KVPOP_ETOOBIG, 99)}
     assert texts[kv.KVPOP_OK] == "success"
     assert "invalid" in texts[kv.KVPOP_EINVAL]
     assert "unsupported" in texts[kv.KVPOP_EUNSUPPORTED]
     assert "HIP" in texts[kv.KVPOP_EHIP]
     assert "unknown" in texts[99]
-    assert len(set(texts.values())) == 5
+    assert "no-allocation" in texts[kv.KVPOP_ETOOBIG]
+    assert len(set(texts.values())) == 6
 
 
 # Fake device addresses: never dereferenced, because every call below must be
@@ -191,6 +193,37 @@ def test_running_topk_argument_checks():
     assert _tk(ev=C_ + 16) == EINVAL                  # eviction output over the cutoff
 
 
+def _tkn(dims=(2, 3, 100), scores=A, lg=None, s=4, w=8, k=5, rank=B_, cut=C_, lab=None, bnd=None, ev=None):
+    d = kv.KvpopTopkDims(*dims) if dims is not None else None
+    return kv.lib().kvpop_running_topk_noalloc(ctypes.byref(d) if d is not None else None, scores, lg, s, w, k,
+                                               rank, cut, lab, bnd, ev, None)
+
+
+def test_running_topk_noalloc_argument_checks():
+    """The no-allocation variant validates like kvpop_running_topk and rejects a
+    problem whose workspace exceeds its scratch array (nothing is launched)."""
+    assert kv.KVPOP_NOALLOC_SCRATCH_BYTES == 32 << 20
+    assert _tkn(dims=None) == EINVAL
+    for dims in [(0, 1, 10), (1, 0, 10), (1, 1, 0)]:
+        assert _tkn(dims=dims) == EINVAL
+    assert _tkn(dims=(1, 1, (1 << 24) + 1)) == EUNS
+    assert _tkn(s=-1) == EINVAL
+    assert _tkn(w=-1) == EINVAL
+    assert _tkn(k=0) == EINVAL
+    assert _tkn(scores=None) == EINVAL
+    assert _tkn(rank=None) == EINVAL
+    assert _tkn(cut=None) == EINVAL
+    assert _tkn(scores=A + 4) == EUNS
+    assert _tkn(cut=B_ + 16) == EINVAL
+    assert _tkn(lab=A + 16) == EINVAL
+    # the largest problems that fit, and the first ones that do not
+    assert kv.kvpop_running_topk_workspace_size(4, 8, 32768) <= kv.KVPOP_NOALLOC_SCRATCH_BYTES
+    assert kv.kvpop_running_topk_workspace_size(1, 8, 131072) <= kv.KVPOP_NOALLOC_SCRATCH_BYTES
+    assert kv.kvpop_running_topk_workspace_size(5, 8, 32768) > kv.KVPOP_NOALLOC_SCRATCH_BYTES
+    assert _tkn(dims=(5, 8, 32768)) == kv.KVPOP_ETOOBIG
+    assert _tkn(dims=(1, 1, 2_000_000)) == kv.KVPOP_ETOOBIG
+
+
 F_, G_ = 0x60000000, 0x70000000
 
 
@@ -228,7 +261,7 @@ def test_forced_hip_error_path(monkeypatch):
     monkeypatch.setenv("KVPOP_TEST_FORCE_EHIP", str(code))
     d = _dims()
     calls = [lambda: _lse(d), lambda: _p2(d), lambda: _tgt(d), lambda: _sc(d), lambda: _tk(),
-             lambda: _sa(d)]
+             lambda: _sa(d), lambda: _tkn()]
     for c in calls:
         assert c() == kv.KVPOP_EHIP
         text = kv.kvpop_strerror(kv.KVPOP_EHIP)
