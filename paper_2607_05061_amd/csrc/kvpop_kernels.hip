@@ -381,21 +381,31 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
 // ---------------------------------------------------------------------------
 // Pass 2: future mass per key.
 //
-// Workgroup = (batch b, KV head h, key block of BK = 4 * NS * 32 keys); wave w owns
-// NS column subtiles of 32 keys whose K rows stay in registers. The workgroup
-// sweeps the query tiles of 32 rows that can see its keys from the last one down;
-// one step stages the tiles of GC query heads of the group in LDS together with
-// their LSE values, and every wave reads them all. Descending order keeps the key
-// blocks of one KV head -- which all end at the last query row -- on the same tile
-// at the same time, so they share it through L2.
+// Workgroup = (batch b, KV head h, key block of BK = 4 * WK keys); wave w owns
+// NSUB key subtiles of 16 (WK = 16 NSUB keys) whose K rows stay in registers as the
+// B operand of v_mfma_f32_16x16x32_bf16. The workgroup sweeps the query tiles of 32
+// rows that can see its keys from the last one down; one step stages the tiles of
+// GC query heads of the group in LDS together with their LSE values, and every wave
+// reads them all. Descending order keeps the key blocks of one KV head -- which all
+// end at the last query row -- on the same tile at the same time, so they share it
+// through L2.
 //
-// Every lane accumulates, for its key column, exp2(acc * c - LSE_d * log2 e) over
-// its 16 query rows of each tile into a per-tile sum and then into a running
-// column sum (a two-level sum keeps the fp32 error near (16 + tiles) ulp). At the
-// end the two half-wave sums of each column are added and written: each workgroup
-// owns its output columns, so results are deterministic, with no atomics. (A
-// small grid splits the query heads of a key block over several workgroups; each
-// still owns its (head, key) outputs and sums them in the same order.)
+// MFMA 16x16x32 lane layout (checked on gfx950): A row m = lane % 16 holds
+// k = 8 (lane / 16) .. +7; B column n = lane % 16 holds the same k range; the 4
+// accumulators of a lane are column n = lane % 16, rows 4 (lane / 16) + r. So k-step
+// s of lane l takes the 16-byte chunk 4 s + l / 16 of the head vector in both
+// operands, a 32-row query tile is two 16-row subtiles (qs), and a lane holds, per
+// head and step, 8 query rows (2 qs x 4 r) of each of its NSUB keys.
+//
+// Per head and step a wave runs 2 NSUB independent MFMA chains of D / 32 k-steps
+// (8 chains at NSUB = 4): no MFMA waits for its predecessor in the chain. Every lane
+// accumulates, for its key columns, exp2(acc * c - LSE_d * log2 e) over its rows of
+// each tile into a per-tile sum and then into a running column sum (a two-level sum
+// keeps the fp32 error near (8 + tiles) ulp). At the end the four lane sums of each
+// column are added and written: each workgroup owns its output columns, so results
+// are deterministic, with no atomics. (A small grid splits the query heads of a key
+// block over several workgroups; each still owns its (head, key) outputs and sums
+// them in the same order.)
 //
 // Query rows beyond T get LSE = +inf in LDS, which zeroes their terms. A per-key
 // bias is factored out of the sum, out_t = exp(bias_t) * sum_d exp(...). Query
@@ -420,24 +430,71 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
 // number of admissible queries). The per-head masses are then written only when
 // `out` is given.
 // ---------------------------------------------------------------------------
-template <int D, int NS, int GC, bool HAS_BIAS, bool EPI>
+
+__device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// A 32-row x D bf16 query tile in LDS for the 16x16x32 layout, stored as
+// 2 * KS4 planes of 1 KB (KS4 = D / 32 k-steps). Plane qs * KS4 + s holds rows
+// 16 qs .. 16 qs + 15, chunks 4 s .. 4 s + 3, lane l's A operand at byte 16 l:
+// row 16 qs + l % 16, chunk 4 s + l / 16. One contiguous, conflict-free 1 KB read
+// per (qs, k-step).
+template <int D>
+struct Tile16 {
+  static constexpr int KS4 = D / 32;
+  static constexpr int PLANES = 2 * KS4;
+  static constexpr int ELEMS = 32 * D;
+  static constexpr int PLANE = 512;  // bf16 elements per plane
+
+  // Byte offset in a row-major [rows, D] matrix of the chunk lane l copies into its
+  // plane slot for query subtile qs (the k-step adds 64 s bytes).
+  static __device__ __forceinline__ int lane_voffset(int lane, int qs) {
+    return (16 * qs + (lane & 15)) * D * 2 + (lane >> 4) * 16;
+  }
+
+  // Copy NP consecutive planes starting at plane p0 of the tile whose first row is
+  // `rows` (`valid` <= 32 rows readable; rows >= valid read as zero) into `lds`.
+  template <int NP>
+  static __device__ __forceinline__ void planes_to_lds(uint16_t* lds, const uint16_t* rows, int valid, int p0,
+                                                       int voff0, int voff1) {
+    const __amdgpu_buffer_rsrc_t r =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(rows), (short)0, valid * D * 2, kRsrcWord3);
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+      const int p = p0 + i, qs = p / KS4, s = p - qs * KS4;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(lds + p * PLANE), 16, qs ? voff1 : voff0, s * 64, 0,
+                                               0);
+    }
+  }
+
+  static __device__ __forceinline__ bf16x8 frag(const uint16_t* lds, int lane, int qs, int s) {
+    return *reinterpret_cast<const bf16x8*>(lds + (qs * KS4 + s) * PLANE + lane * 8);
+  }
+};
+
+template <int D, int NSUB, int GC, bool HAS_BIAS, bool EPI>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2))) void
 future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const float* __restrict__ bias,
                    const float* __restrict__ lse, float* __restrict__ out, int B, int Hq, int Hkv, int T, float c,
                    int window, int hz, float* __restrict__ scores, int agg_mean, float eps, int normalize,
                    int xgroups, int hs) {
-  using TL = Tile<D>;
-  constexpr int KS = TL::KS;
-  constexpr int WK = NS * 32;  // keys per wave
-  constexpr int BK = 4 * WK;   // keys per workgroup
-  constexpr int PPW = GC * KS / 4;  // LDS planes each wave copies per step
-  static_assert(PPW >= 1 && KS % PPW == 0, "plane split");
+  using TL = Tile16<D>;
+  constexpr int KS4 = TL::KS4;
+  constexpr int WK = NSUB * 16;  // keys per wave
+  constexpr int BK = 4 * WK;     // keys per workgroup
+  constexpr int PPW = GC * TL::PLANES / 4;  // LDS planes each wave copies per step
+  static_assert(PPW >= 1 && TL::PLANES % PPW == 0, "plane split");
+  constexpr int NV = 8 * NSUB;              // values per lane, head and step
+  constexpr int SLOTS = 2 * KS4 * NSUB;     // MFMAs per head and step
+  constexpr int V = NV / SLOTS;             // values per MFMA slot
+  static_assert(V * SLOTS == NV, "values per slot");
   __shared__ __attribute__((aligned(16))) uint16_t sq0[GC * TL::ELEMS];
   __shared__ __attribute__((aligned(16))) uint16_t sq1[GC * TL::ELEMS];
   __shared__ __attribute__((aligned(16))) float sl0[GC * 32];
   __shared__ __attribute__((aligned(16))) float sl1[GC * 32];
 
-  const int tid = threadIdx.x, lane = tid & 63, hi = lane >> 5, l32 = lane & 31;
+  const int tid = threadIdx.x, lane = tid & 63, quad = lane >> 4, l16 = lane & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, uniform per wave
   const int G = Hq / Hkv;
   const int nbh = B * Hkv;
@@ -484,16 +541,16 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
 
   // Bias of this lane's key columns: factored out (fac) by the fast sweep, added to
   // every exponent (bl2, log2 units) by the exact sweep. masked: bias -inf.
-  float fac[NS], bl2[NS];
-  bool masked[NS];
+  float fac[NSUB], bl2[NSUB];
+  bool masked[NSUB];
   bool big = false;
 #pragma unroll
-  for (int n = 0; n < NS; ++n) {
+  for (int n = 0; n < NSUB; ++n) {
     fac[n] = 1.f;
     bl2[n] = 0.f;
     masked[n] = false;
     if (HAS_BIAS) {
-      const int j = min(jw + 32 * n + l32, T - 1);
+      const int j = min(jw + 16 * n + l16, T - 1);
       const float bj = bias[j];
       masked[n] = bj == -__builtin_inff();
       bl2[n] = masked[n] ? 0.f : bj * kLog2e;
@@ -502,14 +559,14 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     }
   }
 
-  float aggv[NS];  // running max or sum over query heads (EPI)
+  float aggv[NSUB];  // running max or sum over query heads (EPI)
 #pragma unroll
-  for (int n = 0; n < NS; ++n) aggv[n] = 0.f;
+  for (int n = 0; n < NSUB; ++n) aggv[n] = 0.f;
   auto write_scores = [&]() __attribute__((always_inline)) {
 #pragma unroll
-    for (int n = 0; n < NS; ++n) {
-      const int j = jw + 32 * n + l32;
-      if (hi == 0 && j < T) {
+    for (int n = 0; n < NSUB; ++n) {
+      const int j = jw + 16 * n + l16;
+      if (quad == 0 && j < T) {
         float r = __logf((agg_mean ? aggv[n] / (float)G : aggv[n]) + eps);
         if (normalize) {
           const long long cnt = min((long long)T - 1, (long long)j + hz) - ((long long)j + window) + 1;
@@ -523,11 +580,11 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
   if (nqt == 0) {
     // Every key of the block has an empty query range.
     if (!EPI || out) {
-      for (int g = 0; g < G; ++g) {
+      for (int g = ch * GC; g < G; ++g) {
 #pragma unroll
-        for (int n = 0; n < NS; ++n) {
-          const int j = jw + 32 * n + l32;
-          if (hi == 0 && j < T) out[(size_t)(b * Hq + h * G + g) * T + j] = 0.f;
+        for (int n = 0; n < NSUB; ++n) {
+          const int j = jw + 16 * n + l16;
+          if (quad == 0 && j < T && (hs == 1 || (g / GC) % hs == ch)) out[(size_t)(b * Hq + h * G + g) * T + j] = 0.f;
         }
       }
     }
@@ -538,14 +595,18 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
   // Workgroup-uniform: any key of the block with a large finite bias.
   const bool all_exact = HAS_BIAS && __syncthreads_or(big);
 
-  bf16x8 kf[NS][KS];  // this lane's key rows (B operand), resident for the whole sweep
+  bf16x8 kf[NSUB][KS4];  // this lane's key rows (B operand), resident for the whole sweep
   const uint16_t* Kbh = K + (size_t)bh * T * D;
 #pragma unroll
-  for (int n = 0; n < NS; ++n) load_b_operand<D>(kf[n], Kbh + (size_t)min(jw + 32 * n + l32, T - 1) * D, hi);
+  for (int n = 0; n < NSUB; ++n) {
+    const uint16_t* row = Kbh + (size_t)min(jw + 16 * n + l16, T - 1) * D;
+#pragma unroll
+    for (int s = 0; s < KS4; ++s) kf[n][s] = *reinterpret_cast<const bf16x8*>(row + (4 * s + quad) * 8);
+  }
 
-  const int voff = TL::lane_voffset(lane);
-  const int pg = (w * PPW) / KS;          // the head tile this wave copies
-  const int ps0 = (w * PPW) - pg * KS;    // its first plane
+  const int voff0 = TL::lane_voffset(lane, 0), voff1 = TL::lane_voffset(lane, 1);
+  const int pg = (w * PPW) / TL::PLANES;          // the head tile this wave copies
+  const int pp0 = (w * PPW) - pg * TL::PLANES;    // its first plane
 
   for (int gh0 = h * G + ch * GC; gh0 < (h + 1) * G; gh0 += GC * hs) {
     const size_t head0 = (size_t)(b * Hq + gh0);
@@ -553,8 +614,8 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     // Start the loads of step s: Q tiles straight into LDS, raw LSE into a register.
     auto issue = [&](int s, uint16_t* sq) __attribute__((always_inline)) {
       const int i0 = (qt_hi - s) * 32;
-      TL::template planes_to_lds<PPW>(sq + pg * TL::ELEMS, Q + ((head0 + pg) * T + i0) * D, min(32, T - i0), ps0,
-                                      voff);
+      TL::template planes_to_lds<PPW>(sq + pg * TL::ELEMS, Q + ((head0 + pg) * T + i0) * D, min(32, T - i0), pp0,
+                                      voff0, voff1);
       if (tid < GC * 32) {
         const int i = i0 + (tid & 31);
         stl = i < T ? lse[(head0 + (tid >> 5)) * T + i] : __builtin_inff();
@@ -564,80 +625,98 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
       if (tid < GC * 32) sl[tid] = -stl * kLog2e;
     };
 
-    float colsum[GC][NS];  // fast sweep: column sums; exact sweep: sums relative to mref
-    float mref[GC][NS];    // exact sweep: running maximum of the exponents (log2 units)
+    float colsum[GC][NSUB];  // fast sweep: column sums; exact sweep: sums relative to mref
+    float mref[GC][NSUB];    // exact sweep: running maximum of the exponents (log2 units)
 
-    auto read_nl = [&](const float* sl, int g, float (&nl)[16]) {
+    // -LSE_d log2 e of this lane's rows 16 qs + 4 quad + r of head g: nl[4 qs + r].
+    auto read_nl = [&](const float* sl, int g, float (&nl)[8]) __attribute__((always_inline)) {
 #pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        const f32x4 v = *reinterpret_cast<const f32x4*>(&sl[g * 32 + 8 * g4 + 4 * hi]);
-        nl[4 * g4 + 0] = v[0];
-        nl[4 * g4 + 1] = v[1];
-        nl[4 * g4 + 2] = v[2];
-        nl[4 * g4 + 3] = v[3];
+      for (int qs = 0; qs < 2; ++qs) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(&sl[g * 32 + 16 * qs + 4 * quad]);
+        nl[4 * qs + 0] = v[0];
+        nl[4 * qs + 1] = v[1];
+        nl[4 * qs + 2] = v[2];
+        nl[4 * qs + 3] = v[3];
       }
-    };
-    auto accumulate = [&](const f32x16& acc, const float (&nl)[16], float& cs) {
-      float ts = 0.f;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) ts += exp2_fast(__builtin_fmaf(acc[r], c, nl[r]));
-      cs += ts;
     };
 
     // Fully admissible step, as a software pipeline over the GC heads with a fixed
     // issue order (the scheduling barriers stop the compiler from regrouping it).
-    // Head g's unit runs the NS MFMA chains of its key subtiles interleaved k-step
-    // by k-step, so each A fragment read from LDS feeds NS MFMAs; right after those
-    // MFMAs the fragment register is refilled with head g + 1's operand (used a
-    // whole unit later, hiding the LDS latency). Each MFMA is followed by the
-    // exp/accumulate work of one key subtile of head g - 1, whose accumulators
-    // completed during the previous unit, so the VALU work issues while the MFMAs
-    // run.
+    // Head g's unit runs its 2 NSUB MFMA chains k-step by k-step, so each A fragment
+    // read from LDS feeds NSUB MFMAs; right after those the fragment register is
+    // refilled with head g + 1's operand (used a whole unit later, hiding the LDS
+    // latency). Each MFMA slot also issues the VALU work of head g - 1's values,
+    // itself pipelined over three slots: the fma of value v, the exp of value v - V
+    // and the add of value v - 2 V, so that the three instructions after one MFMA
+    // never wait for each other. Values run key-subtile fastest, so consecutive
+    // adds go to different partial sums.
     auto full_step = [&](const uint16_t* sq, const float* sl) __attribute__((always_inline)) {
-      constexpr int EPK = 16 / KS;  // elements per subtile of the previous head per k-step
-      bf16x8 fr[KS];
-      float nl[2][16];
-      f32x16 acc_prev[NS];
+      bf16x8 fr[2][KS4];
+      float nl[2][8];
+      f32x4 acc_prev[2][NSUB];
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) fr[ks] = TL::frag(sq, lane, ks);
+      for (int qs = 0; qs < 2; ++qs)
+#pragma unroll
+        for (int s = 0; s < KS4; ++s) fr[qs][s] = TL::frag(sq, lane, qs, s);
       read_nl(sl, 0, nl[0]);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int g = 0; g <= GC; ++g) {
         if (g > 0 && g < GC) read_nl(sl, g, nl[g & 1]);
-        f32x16 acc[NS];
+        f32x4 acc[2][NSUB];
 #pragma unroll
-        for (int n = 0; n < NS; ++n) acc[n] = f32x16{};
-        float ts[NS][2];
+        for (int qs = 0; qs < 2; ++qs)
 #pragma unroll
-        for (int n = 0; n < NS; ++n) ts[n][0] = ts[n][1] = 0.f;
+          for (int n = 0; n < NSUB; ++n) acc[qs][n] = f32x4{};
+        float ts[NSUB];
+        float y[NV], x[NV];
+        const float(&pnl)[8] = nl[(g + 1) & 1];  // head g - 1's normalisers
+        // value v of head g - 1: key subtile v % NSUB, row slot v / NSUB = 4 qs + r
+        auto val = [&](int v) __attribute__((always_inline)) {
+          const int n = v % NSUB, rr = v / NSUB;
+          return __builtin_fmaf(acc_prev[rr >> 2][n][rr & 3], c, pnl[rr]);
+        };
+        auto add = [&](int v) __attribute__((always_inline)) {
+          const int n = v % NSUB;
+          ts[n] = v < NSUB ? x[v] : ts[n] + x[v];  // the first terms seed the sums
+        };
+        int slot = 0;
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
+        for (int s = 0; s < KS4; ++s) {
 #pragma unroll
-          for (int n = 0; n < NS; ++n) {
-            // one MFMA, then the exponentials of one subtile of the previous head
-            if (g < GC) {
-              acc[n] = mfma32(fr[ks], kf[n][ks], acc[n]);
-              if (n == NS - 1 && g + 1 < GC) fr[ks] = TL::frag(sq + (g + 1) * TL::ELEMS, lane, ks);
-            }
-            if (g > 0) {
+          for (int qs = 0; qs < 2; ++qs) {
 #pragma unroll
-              for (int e = 0; e < EPK; ++e) {
-                const int r = ks * EPK + e;
-                const float x = exp2_fast(__builtin_fmaf(acc_prev[n][r], c, nl[(g - 1) & 1][r]));
-                // The first terms seed the partial sums (0 + x is not folded away).
-                ts[n][e & 1] = r < 2 ? x : ts[n][e & 1] + x;
+            for (int n = 0; n < NSUB; ++n) {
+              if (g < GC) {
+                acc[qs][n] = mfma16(fr[qs][s], kf[n][s], acc[qs][n]);
+                if (n == NSUB - 1 && g + 1 < GC) fr[qs][s] = TL::frag(sq + (g + 1) * TL::ELEMS, lane, qs, s);
               }
+              if (g > 0) {
+#pragma unroll
+                for (int e = 0; e < V; ++e) {
+                  const int v = slot * V + e;
+                  y[v] = val(v);
+                  if (v >= V) x[v - V] = exp2_fast(y[v - V]);
+                  if (v >= 2 * V) add(v - 2 * V);
+                }
+              }
+              ++slot;
+              __builtin_amdgcn_sched_barrier(0);
             }
-            __builtin_amdgcn_sched_barrier(0);
           }
         }
         if (g > 0) {
 #pragma unroll
-          for (int n = 0; n < NS; ++n) colsum[g - 1][n] += ts[n][0] + ts[n][1];
+          for (int v = NV - V; v < NV; ++v) x[v] = exp2_fast(y[v]);
+#pragma unroll
+          for (int v = NV - 2 * V; v < NV; ++v) add(v);
+#pragma unroll
+          for (int n = 0; n < NSUB; ++n) colsum[g - 1][n] += ts[n];
         }
 #pragma unroll
-        for (int n = 0; n < NS; ++n) acc_prev[n] = acc[n];
+        for (int qs = 0; qs < 2; ++qs)
+#pragma unroll
+          for (int n = 0; n < NSUB; ++n) acc_prev[qs][n] = acc[qs][n];
       }
     };
 
@@ -645,39 +724,35 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     // the band (skipped), inside it (summed without a mask) or across its edge (each
     // pair masked by window <= i - j <= hz).
     auto edge_step = [&](const uint16_t* sq, const float* sl, int i0) __attribute__((always_inline)) {
-      bool act[NS], inside[NS];
+      bool act[NSUB], inside[NSUB];
 #pragma unroll
-      for (int n = 0; n < NS; ++n) {
-        const int dlo = i0 - (jw + 32 * n + 31), dhi = i0 + 31 - (jw + 32 * n);
+      for (int n = 0; n < NSUB; ++n) {
+        const int dlo = i0 - (jw + 16 * n + 15), dhi = i0 + 31 - (jw + 16 * n);
         act[n] = !(dhi < window || dlo > hz);
         inside[n] = dlo >= window && dhi <= hz;
       }
 #pragma unroll
       for (int g = 0; g < GC; ++g) {
-        float nl[16];
+        float nl[8];
         read_nl(sl, g, nl);
 #pragma unroll
-        for (int n = 0; n < NS; ++n) {
+        for (int n = 0; n < NSUB; ++n) {
           if (!act[n]) continue;
-          f32x16 acc = f32x16{};
+          f32x4 acc[2];
 #pragma unroll
-          for (int ks = 0; ks < KS; ++ks) acc = mfma32(TL::frag(sq + g * TL::ELEMS, lane, ks), kf[n][ks], acc);
+          for (int qs = 0; qs < 2; ++qs) {
+            acc[qs] = f32x4{};
+#pragma unroll
+            for (int s = 0; s < KS4; ++s) acc[qs] = mfma16(TL::frag(sq + g * TL::ELEMS, lane, qs, s), kf[n][s], acc[qs]);
+          }
           float ts[2];
-          if (inside[n]) {
+          const int base = i0 + 4 * quad - (jw + 16 * n + l16);
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const float x = exp2_fast(__builtin_fmaf(acc[r], c, nl[r]));
-              ts[r & 1] = r < 2 ? x : ts[r & 1] + x;  // the first terms seed the sums
-            }
-          } else {
-            const int base = i0 + 4 * hi - (jw + 32 * n + l32);
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const int d = base + 8 * (r >> 2) + (r & 3);
-              const float e = exp2_fast(__builtin_fmaf(acc[r], c, nl[r]));
-              const float x = (d >= window && d <= hz) ? e : 0.f;
-              ts[r & 1] = r < 2 ? x : ts[r & 1] + x;
-            }
+          for (int rr = 0; rr < 8; ++rr) {
+            const int d = base + 16 * (rr >> 2) + (rr & 3);
+            const float e = exp2_fast(__builtin_fmaf(acc[rr >> 2][rr & 3], c, nl[rr]));
+            const float xv = (inside[n] || (d >= window && d <= hz)) ? e : 0.f;
+            ts[rr & 1] = rr < 2 ? xv : ts[rr & 1] + xv;  // the first terms seed the sums
           }
           colsum[g][n] += ts[0] + ts[1];
         }
@@ -688,31 +763,35 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     // LSE_d log2 e + bias_t log2 e, and per column an online update of (mref, colsum)
     // as in online softmax. A summand of +inf (LSE_d = -inf) makes the mass +inf.
     auto exact_step = [&](const uint16_t* sq, const float* sl, int i0) __attribute__((always_inline)) {
-      bool act[NS];
+      bool act[NSUB];
 #pragma unroll
-      for (int n = 0; n < NS; ++n) {
-        const int dlo = i0 - (jw + 32 * n + 31), dhi = i0 + 31 - (jw + 32 * n);
+      for (int n = 0; n < NSUB; ++n) {
+        const int dlo = i0 - (jw + 16 * n + 15), dhi = i0 + 31 - (jw + 16 * n);
         act[n] = !(dhi < window || dlo > hz);
       }
 #pragma unroll
       for (int g = 0; g < GC; ++g) {
-        float nl[16];
+        float nl[8];
         read_nl(sl, g, nl);
 #pragma unroll
-        for (int n = 0; n < NS; ++n) {
+        for (int n = 0; n < NSUB; ++n) {
           if (!act[n]) continue;
-          f32x16 acc = f32x16{};
+          f32x4 acc[2];
 #pragma unroll
-          for (int ks = 0; ks < KS; ++ks) acc = mfma32(TL::frag(sq + g * TL::ELEMS, lane, ks), kf[n][ks], acc);
-          const int base = i0 + 4 * hi - (jw + 32 * n + l32);
-          float x[16];
+          for (int qs = 0; qs < 2; ++qs) {
+            acc[qs] = f32x4{};
+#pragma unroll
+            for (int s = 0; s < KS4; ++s) acc[qs] = mfma16(TL::frag(sq + g * TL::ELEMS, lane, qs, s), kf[n][s], acc[qs]);
+          }
+          const int base = i0 + 4 * quad - (jw + 16 * n + l16);
+          float xv[8];
           float tmax = -__builtin_inff();
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int d = base + 8 * (r >> 2) + (r & 3);
-            const float xr = __builtin_fmaf(acc[r], c, nl[r]) + bl2[n];
-            x[r] = (d >= window && d <= hz) ? xr : -__builtin_inff();
-            tmax = fmaxf(tmax, x[r]);
+          for (int rr = 0; rr < 8; ++rr) {
+            const int d = base + 16 * (rr >> 2) + (rr & 3);
+            const float xr = __builtin_fmaf(acc[rr >> 2][rr & 3], c, nl[rr]) + bl2[n];
+            xv[rr] = (d >= window && d <= hz) ? xr : -__builtin_inff();
+            tmax = fmaxf(tmax, xv[rr]);
           }
           const float mn = fmaxf(mref[g][n], tmax);
           if (mn == __builtin_inff()) {
@@ -721,7 +800,7 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
           } else if (mn > -__builtin_inff()) {
             float e = 0.f;
 #pragma unroll
-            for (int r = 0; r < 16; ++r) e += exp2_fast(x[r] - mn);
+            for (int rr = 0; rr < 8; ++rr) e += exp2_fast(xv[rr] - mn);
             colsum[g][n] = colsum[g][n] * exp2_fast(mref[g][n] - mn) + e;
             mref[g][n] = mn;
           }
@@ -748,23 +827,21 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
 #pragma unroll
     for (int g = 0; g < GC; ++g)
 #pragma unroll
-      for (int n = 0; n < NS; ++n) colsum[g][n] = 0.f;
+      for (int n = 0; n < NSUB; ++n) colsum[g][n] = 0.f;
     bool bad = false;
     if (!all_exact) {
-      if (nqt > 0) {
-        issue(0, sq0);
-        commit(sl0);
-        __syncthreads();
-        for (int s = 0; s < nqt; s += 2) {
-          step(s, sq0, sl0, sq1, sl1);
-          if (s + 1 < nqt) step(s + 1, sq1, sl1, sq0, sl0);
-        }
+      issue(0, sq0);
+      commit(sl0);
+      __syncthreads();
+      for (int s = 0; s < nqt; s += 2) {
+        step(s, sq0, sl0, sq1, sl1);
+        if (s + 1 < nqt) step(s + 1, sq1, sl1, sq0, sl0);
       }
-      // Each half-wave sum at most 2^63 keeps the column's sum within 2^64.
+      // Each of the four lane sums at most 2^62 keeps the column's sum within 2^64.
 #pragma unroll
       for (int g = 0; g < GC; ++g)
 #pragma unroll
-        for (int n = 0; n < NS; ++n) bad |= !masked[n] && !(colsum[g][n] <= 0.5f * kOverflow);
+        for (int n = 0; n < NSUB; ++n) bad |= !masked[n] && !(colsum[g][n] <= 0.25f * kOverflow);
     }
 
     // Block-wide: a large bias, or a column sum out of the safe range, takes the
@@ -784,54 +861,56 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
 #pragma unroll
       for (int g = 0; g < GC; ++g)
 #pragma unroll
-        for (int n = 0; n < NS; ++n) {
+        for (int n = 0; n < NSUB; ++n) {
           colsum[g][n] = 0.f;
           mref[g][n] = -__builtin_inff();
         }
-      if (nqt > 0) {
-        issue(0, sq0);
-        commit(sl0);
-        __syncthreads();
-        for (int s = 0; s < nqt; s += 2) {
-          xstep(s, sq0, sl0, sq1, sl1);
-          if (s + 1 < nqt) xstep(s + 1, sq1, sl1, sq0, sl0);
-        }
+      issue(0, sq0);
+      commit(sl0);
+      __syncthreads();
+      for (int s = 0; s < nqt; s += 2) {
+        xstep(s, sq0, sl0, sq1, sl1);
+        if (s + 1 < nqt) xstep(s + 1, sq1, sl1, sq0, sl0);
       }
-      // Combine the half-wave (mref, sum) pairs and write exp2(m + log2 sum).
+      // Merge the four lanes' (mref, sum) pairs of each column and write
+      // exp2(m + log2 sum).
 #pragma unroll
       for (int g = 0; g < GC; ++g) {
 #pragma unroll
-        for (int n = 0; n < NS; ++n) {
-          const float mo = __shfl_xor(mref[g][n], 32);
-          const float so = __shfl_xor(colsum[g][n], 32);
-          const float mm = fmaxf(mref[g][n], mo);
+        for (int n = 0; n < NSUB; ++n) {
+          float m = mref[g][n], sm = colsum[g][n];
+#pragma unroll
+          for (int sh = 16; sh <= 32; sh *= 2) {
+            const float mo = __shfl_xor(m, sh);
+            const float so = __shfl_xor(sm, sh);
+            const float mm = fmaxf(m, mo);
+            if (mm == __builtin_inff()) {
+              sm = 1.f;
+            } else if (mm > -__builtin_inff()) {
+              sm = sm * exp2_fast(m - mm) + so * exp2_fast(mo - mm);
+            }
+            m = mm;
+          }
           float v = 0.f;
-          if (mm == __builtin_inff()) {
-            v = mm;
-          } else if (mm > -__builtin_inff()) {
-            const float tot = colsum[g][n] * exp2_fast(mref[g][n] - mm) + so * exp2_fast(mo - mm);
-            v = exp2_fast(mm + __log2f(tot));
-          }
+          if (m == __builtin_inff()) v = m;
+          else if (m > -__builtin_inff()) v = exp2_fast(m + __log2f(sm));
           if (masked[n]) v = 0.f;
-          const int j = jw + 32 * n + l32;
-          if (hi == 0 && j < T && (!EPI || out)) {
-            out[(head0 + g) * T + j] = v;
-          }
+          const int j = jw + 16 * n + l16;
+          if (quad == 0 && j < T && (!EPI || out)) out[(head0 + g) * T + j] = v;
           if (EPI) aggv[n] = agg_mean ? aggv[n] + v : fmaxf(aggv[n], v);
         }
       }
     } else {
-      // Combine the half-wave sums and write this chunk's columns.
+      // Combine the four lane sums of each column and write this chunk's columns.
 #pragma unroll
       for (int g = 0; g < GC; ++g) {
 #pragma unroll
-        for (int n = 0; n < NS; ++n) {
-          float v = colsum[g][n] + __shfl_xor(colsum[g][n], 32);
+        for (int n = 0; n < NSUB; ++n) {
+          float v = colsum[g][n] + __shfl_xor(colsum[g][n], 16);
+          v += __shfl_xor(v, 32);
           if (HAS_BIAS) v = masked[n] ? 0.f : v * fac[n];
-          const int j = jw + 32 * n + l32;
-          if (hi == 0 && j < T && (!EPI || out)) {
-            out[(head0 + g) * T + j] = v;
-          }
+          const int j = jw + 16 * n + l16;
+          if (quad == 0 && j < T && (!EPI || out)) out[(head0 + g) * T + j] = v;
           if (EPI) aggv[n] = agg_mean ? aggv[n] + v : fmaxf(aggv[n], v);
         }
       }
@@ -868,9 +947,9 @@ int launch_p1_d(const Launch& L) {
   return launch_p1_b<D, 1>(L);
 }
 
-template <int D, int NS, int GC, bool HB, bool EPI>
+template <int D, int NSUB, int GC, bool HB, bool EPI>
 int launch_p2(const Launch& L, int hs) {
-  constexpr int BK = 4 * NS * 32;
+  constexpr int BK = 4 * NSUB * 16;
   const int nkb = (L.T + BK - 1) / BK;
   const long long grid = (long long)nkb * L.B * L.Hkv;
   const float c = L.scale * kLog2e;
@@ -884,23 +963,23 @@ int launch_p2(const Launch& L, int hs) {
     const int ng = nbh / 8;
     xgroups = ng % 2 == 0 && (long long)ng * nkb >= 4 * 64 ? ng / 2 : ng;
   }
-  hipLaunchKernelGGL((future_mass_kernel<D, NS, GC, HB, EPI>), dim3((unsigned)(grid * hs)), dim3(256), 0,
+  hipLaunchKernelGGL((future_mass_kernel<D, NSUB, GC, HB, EPI>), dim3((unsigned)(grid * hs)), dim3(256), 0,
                      (hipStream_t)L.stream, reinterpret_cast<const uint16_t*>(L.q),
                      reinterpret_cast<const uint16_t*>(L.k), L.bias, L.lse, L.out, L.B, L.Hq, L.Hkv, L.T, c, L.window,
                      hz, L.scores, L.agg, L.eps, L.normalize, hs > 1 ? 0 : xgroups, hs);
   return (int)hipGetLastError();
 }
 
-template <int D, int NS, int GC>
+template <int D, int NSUB, int GC>
 int launch_p2_b(const Launch& L, int hs) {
-  if (L.scores) return L.bias ? launch_p2<D, NS, GC, true, true>(L, 1) : launch_p2<D, NS, GC, false, true>(L, 1);
-  return L.bias ? launch_p2<D, NS, GC, true, false>(L, hs) : launch_p2<D, NS, GC, false, false>(L, hs);
+  if (L.scores) return L.bias ? launch_p2<D, NSUB, GC, true, true>(L, 1) : launch_p2<D, NSUB, GC, false, true>(L, 1);
+  return L.bias ? launch_p2<D, NSUB, GC, true, false>(L, hs) : launch_p2<D, NSUB, GC, false, false>(L, hs);
 }
 
-template <int D, int NS>
+template <int D, int NSUB>
 int launch_p2_gc(const Launch& L) {
   const int G = L.Hq / L.Hkv;
-  constexpr int BK = 4 * NS * 32;
+  constexpr int BK = 4 * NSUB * 16;
   const long long grid = (long long)((L.T + BK - 1) / BK) * L.B * L.Hkv;
   // Under 2048 workgroups (8 per CU) with a long band the heaviest key blocks set
   // the time: the query heads of each (key block, group) are then split over
@@ -910,21 +989,22 @@ int launch_p2_gc(const Launch& L) {
   // not pay.
   const bool long_band = L.horizon < 0 || L.horizon >= L.T / 2;
   if (!L.scores && grid < 2048 && long_band && G > 1) {
-    if (grid >= 512 && G % 2 == 0) return launch_p2_b<D, NS, 2>(L, G / 2);
-    return launch_p2_b<D, NS, 1>(L, G);
+    if (grid >= 512 && G % 2 == 0) return launch_p2_b<D, NSUB, 2>(L, G / 2);
+    return launch_p2_b<D, NSUB, 1>(L, G);
   }
   // Query heads per step: the largest of 4, 2, 1 that divides G.
-  if (G % 4 == 0) return launch_p2_b<D, NS, 4>(L, 1);
-  if (G % 2 == 0) return launch_p2_b<D, NS, 2>(L, 1);
-  return launch_p2_b<D, NS, 1>(L, 1);
+  if (G % 4 == 0) return launch_p2_b<D, NSUB, 4>(L, 1);
+  if (G % 2 == 0) return launch_p2_b<D, NSUB, 2>(L, 1);
+  return launch_p2_b<D, NSUB, 1>(L, 1);
 }
 
 template <int D>
 int launch_p2_d(const Launch& L) {
-  // Two key subtiles per wave unless that leaves fewer than ~2 workgroups per CU.
+  // Four 16-key subtiles per wave (256 keys per workgroup) unless that leaves fewer
+  // than ~2 workgroups per CU; then two (128 keys).
   const long long wg2 = (long long)L.B * L.Hkv * ((L.T + 255) / 256);
-  if (wg2 >= 512) return launch_p2_gc<D, 2>(L);
-  return launch_p2_gc<D, 1>(L);
+  if (wg2 >= 512) return launch_p2_gc<D, 4>(L);
+  return launch_p2_gc<D, 2>(L);
 }
 
 }  // namespace
