@@ -118,6 +118,21 @@ int kvpop_future_attn_from_lse(const kvpop_dims* dims, const void* q, const void
                                const float* key_bias, const float* lse, int32_t window,
                                int32_t horizon, float* out, void* stream);
 
+/* Pass 2 for one or two bands of the same keys from one normaliser, in one sweep
+ * (App. B.2: the target with a finite lookahead L and without one, from the same
+ * LSE): for b < n_bands,
+ *   outs[b][b', qh, t] = sum_{d in band_b(t)} exp(l(d, t) - lse[b', qh, d]),
+ * band_b(t) = { d : t + windows[b] <= d <= min(T - 1, t + horizons[b]) }, each exactly
+ * as kvpop_future_attn_from_lse computes it (same guard), up to fp32 summation
+ * order. Each logit and exponential is evaluated once and added to every band that
+ * holds the pair, so a band inside another costs almost nothing.
+ * n_bands: 1 or 2. windows, horizons: host arrays of n_bands entries (the rules of
+ * kvpop_future_attn_from_lse). outs: host array of n_bands device pointers to fp32
+ * [B,Hq,T] outputs, which must not overlap each other or any input. */
+int kvpop_future_attn_bands(const kvpop_dims* dims, const void* q, const void* k, const float* key_bias,
+                            const float* lse, int32_t n_bands, const int32_t* windows, const int32_t* horizons,
+                            float* const* outs, void* stream);
+
 /* Both passes: kvpop_row_lse into lse_ws, then kvpop_future_attn_from_lse from it.
  * lse_ws: caller-allocated fp32 [B,Hq,T]; it holds the dense LSE on completion. */
 int kvpop_future_attn_target(const kvpop_dims* dims, const void* q, const void* k,

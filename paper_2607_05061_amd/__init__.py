@@ -25,7 +25,7 @@ __all__ = [
     "lib", "lib_path", "kvpop_row_lse", "kvpop_future_attn_from_lse", "kvpop_future_attn_target",
     "kvpop_future_attn_scores", "kvpop_strerror", "kvpop_abi_version", "KVPOP_AGG_MAX", "KVPOP_AGG_MEAN",
     "KvpopTopkDims", "kvpop_running_topk", "kvpop_running_topk_workspace_size", "kvpop_sparse_attn_fwd",
-    "kvpop_running_topk_noalloc", "KVPOP_ETOOBIG", "KVPOP_NOALLOC_SCRATCH_BYTES",
+    "kvpop_running_topk_noalloc", "KVPOP_ETOOBIG", "KVPOP_NOALLOC_SCRATCH_BYTES", "kvpop_future_attn_bands",
 ]
 
 KVPOP_OK = 0
@@ -84,6 +84,9 @@ def lib() -> ctypes.CDLL:
         L.kvpop_row_lse.restype = ctypes.c_int
         L.kvpop_future_attn_from_lse.argtypes = [D, P, P, P, P, I32, I32, P, P]
         L.kvpop_future_attn_from_lse.restype = ctypes.c_int
+        L.kvpop_future_attn_bands.argtypes = [D, P, P, P, P, I32, ctypes.POINTER(I32), ctypes.POINTER(I32),
+                                              ctypes.POINTER(P), P]
+        L.kvpop_future_attn_bands.restype = ctypes.c_int
         L.kvpop_future_attn_target.argtypes = [D, P, P, P, I32, I32, P, P, P]
         L.kvpop_future_attn_target.restype = ctypes.c_int
         L.kvpop_future_attn_scores.argtypes = [D, P, P, P, P, I32, I32, I32, F, I32, P, P, P]
@@ -199,6 +202,34 @@ def kvpop_future_attn_from_lse(q, k, lse, scale: float, window: int = 0, horizon
     if st != KVPOP_OK:
         raise KvpopError(st, "kvpop_future_attn_from_lse")
     return out
+
+
+def kvpop_future_attn_bands(q, k, lse, scale: float, bands, key_bias=None, outs=None, stream=None):
+    """Pass 2 for one or two (window, horizon) bands from one normaliser in one sweep;
+    returns a list of fp32 [B, Hq, T] masses, one per band."""
+    torch = _torch()
+    d = _dims(q, k, scale)
+    qp, kp, bp = _prep_inputs(q, k, key_bias)
+    _check_tensor(lse, "lse", torch.float32, q.device)
+    shape = (d.batch, d.n_q_heads, d.seq_len)
+    if tuple(lse.shape) != shape:
+        raise ValueError("lse must be [B, Hq, T]")
+    bands = [(int(a), int(b)) for a, b in bands]
+    if not 1 <= len(bands) <= 2:
+        raise ValueError("one or two bands")
+    outs = [None] * len(bands) if outs is None else list(outs)
+    if len(outs) != len(bands):
+        raise ValueError("one output per band")
+    outs = [_prep_out(o, "outs[%d]" % i, shape, q.device) for i, o in enumerate(outs)]
+    n = len(bands)
+    win = (ctypes.c_int32 * n)(*[b[0] for b in bands])
+    hor = (ctypes.c_int32 * n)(*[b[1] for b in bands])
+    ptr = (ctypes.c_void_p * n)(*[o.data_ptr() for o in outs])
+    st = lib().kvpop_future_attn_bands(ctypes.byref(d), qp, kp, bp, lse.data_ptr(), n, win, hor, ptr,
+                                       _stream_ptr(stream, q.device))
+    if st != KVPOP_OK:
+        raise KvpopError(st, "kvpop_future_attn_bands")
+    return outs
 
 
 def kvpop_future_attn_target(q, k, scale: float, window: int = 0, horizon: int = -1, key_bias=None,

@@ -223,6 +223,35 @@ int kvpop_future_attn_from_lse(const kvpop_dims* dims, const void* q, const void
   return launch([&] { return kvpop::launch_future_mass(L); });
 }
 
+int kvpop_future_attn_bands(const kvpop_dims* dims, const void* q, const void* k, const float* key_bias,
+                            const float* lse, int32_t n_bands, const int32_t* windows, const int32_t* horizons,
+                            float* const* outs, void* stream) {
+  Sizes sz;
+  int st = check_inputs(dims, q, k, key_bias, &sz);
+  if (st != KVPOP_OK) return st;
+  if (!lse) return KVPOP_EINVAL;
+  if (!aligned16(lse)) return KVPOP_EUNSUPPORTED;
+  if (n_bands < 1 || n_bands > 2 || !windows || !horizons || !outs) return KVPOP_EINVAL;
+  for (int i = 0; i < n_bands; ++i) {
+    st = check_band(windows[i], horizons[i]);
+    if (st != KVPOP_OK) return st;
+    st = check_output(outs[i], sz.row_elems * 4, sz, dims, q, k, key_bias, lse, sz.row_elems * 4);
+    if (st != KVPOP_OK) return st;
+  }
+  if (n_bands == 2 && overlap(outs[0], sz.row_elems * 4, outs[1], sz.row_elems * 4)) return KVPOP_EINVAL;
+  kvpop::Launch L = make_launch(dims, q, k, key_bias, stream);
+  L.lse = lse;
+  L.out = outs[0];
+  L.window = windows[0];
+  L.horizon = horizons[0];
+  if (n_bands == 2) {
+    L.out1 = outs[1];
+    L.window1 = windows[1];
+    L.horizon1 = horizons[1];
+  }
+  return launch([&] { return kvpop::launch_future_mass(L); });
+}
+
 int kvpop_future_attn_scores(const kvpop_dims* dims, const void* q, const void* k, const float* key_bias,
                              const float* lse, int32_t window, int32_t horizon, int32_t agg, float eps,
                              int32_t normalize, float* out, float* scores, void* stream) {

@@ -16,6 +16,11 @@ struct Launch {
   float scale;
   int32_t window;      // pass 2 only
   int32_t horizon;     // pass 2 only; < 0 = unbounded
+  // Pass 2 with a second band (out1 != nullptr): its masses go to out1, from the
+  // same sweep.
+  float* out1;         // fp32 [B, Hq, T] or nullptr
+  int32_t window1;
+  int32_t horizon1;
   // Pass 2 target epilogue (scores != nullptr): per KV head and key,
   // log(agg_g out + eps) - (normalize ? log N_t : 0); agg 0 = max, 1 = mean.
   float* scores;       // fp32 [B, Hkv, T] or nullptr

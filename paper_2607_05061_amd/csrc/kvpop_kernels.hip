@@ -40,6 +40,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 
 #include "kvpop_internal.h"
 
@@ -473,12 +475,13 @@ struct Tile16 {
   }
 };
 
-template <int D, int NSUB, int GC, bool HAS_BIAS, bool EPI>
+template <int D, int NSUB, int GC, bool HAS_BIAS, bool EPI, int NB>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2))) void
 future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const float* __restrict__ bias,
                    const float* __restrict__ lse, float* __restrict__ out, int B, int Hq, int Hkv, int T, float c,
                    int window, int hz, float* __restrict__ scores, int agg_mean, float eps, int normalize,
-                   int xgroups, int hs) {
+                   int xgroups, int hs, int window1, int hz1, float* __restrict__ out1) {
+  static_assert(NB == 1 || (NB == 2 && !EPI), "a second band only without the epilogue");
   using TL = Tile16<D>;
   constexpr int KS4 = TL::KS4;
   constexpr int WK = NSUB * 16;  // keys per wave
@@ -531,8 +534,11 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
   const int jw = j0 + w * WK;
 
   // Query rows that can reach any key of the block: [j0 + window, j0 + BK - 1 + hz] within [0, T).
-  const long long r_lo = (long long)j0 + window;
-  const long long r_hi = min((long long)T - 1, (long long)j0 + BK - 1 + hz);
+  // With a second band, the union of the two bands' ranges.
+  const int wlo = NB == 2 ? min(window, window1) : window;
+  const int hhi = NB == 2 ? max(hz, hz1) : hz;
+  const long long r_lo = (long long)j0 + wlo;
+  const long long r_hi = min((long long)T - 1, (long long)j0 + BK - 1 + hhi);
   int qt_hi = 0, nqt = 0;
   if (r_lo <= r_hi) {
     qt_hi = (int)(r_hi / 32);
@@ -584,7 +590,10 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
 #pragma unroll
         for (int n = 0; n < NSUB; ++n) {
           const int j = jw + 16 * n + l16;
-          if (quad == 0 && j < T && (hs == 1 || (g / GC) % hs == ch)) out[(size_t)(b * Hq + h * G + g) * T + j] = 0.f;
+          if (quad == 0 && j < T && (hs == 1 || (g / GC) % hs == ch)) {
+            out[(size_t)(b * Hq + h * G + g) * T + j] = 0.f;
+            if (NB == 2) out1[(size_t)(b * Hq + h * G + g) * T + j] = 0.f;
+          }
         }
       }
     }
@@ -626,6 +635,7 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     };
 
     float colsum[GC][NSUB];  // fast sweep: column sums; exact sweep: sums relative to mref
+    float colsum1[GC][NSUB]; // fast sweep, second band
     float mref[GC][NSUB];    // exact sweep: running maximum of the exponents (log2 units)
 
     // -LSE_d log2 e of this lane's rows 16 qs + 4 quad + r of head g: nl[4 qs + r].
@@ -650,7 +660,9 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     // and the add of value v - 2 V, so that the three instructions after one MFMA
     // never wait for each other. Values run key-subtile fastest, so consecutive
     // adds go to different partial sums.
-    auto full_step = [&](const uint16_t* sq, const float* sl) __attribute__((always_inline)) {
+    // BANDS: bit b set = band b takes this step's sums (always 1 with one band).
+    auto full_step = [&](auto bands_c, const uint16_t* sq, const float* sl) __attribute__((always_inline)) {
+      constexpr int BANDS = decltype(bands_c)::value;
       bf16x8 fr[2][KS4];
       float nl[2][8];
       f32x4 acc_prev[2][NSUB];
@@ -711,7 +723,10 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
 #pragma unroll
           for (int v = NV - 2 * V; v < NV; ++v) add(v);
 #pragma unroll
-          for (int n = 0; n < NSUB; ++n) colsum[g - 1][n] += ts[n];
+          for (int n = 0; n < NSUB; ++n) {
+            if (BANDS & 1) colsum[g - 1][n] += ts[n];
+            if (BANDS & 2) colsum1[g - 1][n] += ts[n];
+          }
         }
 #pragma unroll
         for (int qs = 0; qs < 2; ++qs)
@@ -724,12 +739,14 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     // the band (skipped), inside it (summed without a mask) or across its edge (each
     // pair masked by window <= i - j <= hz).
     auto edge_step = [&](const uint16_t* sq, const float* sl, int i0) __attribute__((always_inline)) {
-      bool act[NSUB], inside[NSUB];
+      bool act[NSUB], inside[NSUB], act1[NSUB], inside1[NSUB];
 #pragma unroll
       for (int n = 0; n < NSUB; ++n) {
         const int dlo = i0 - (jw + 16 * n + 15), dhi = i0 + 31 - (jw + 16 * n);
         act[n] = !(dhi < window || dlo > hz);
         inside[n] = dlo >= window && dhi <= hz;
+        act1[n] = NB == 2 && !(dhi < window1 || dlo > hz1);
+        inside1[n] = NB == 2 && dlo >= window1 && dhi <= hz1;
       }
 #pragma unroll
       for (int g = 0; g < GC; ++g) {
@@ -737,7 +754,7 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
         read_nl(sl, g, nl);
 #pragma unroll
         for (int n = 0; n < NSUB; ++n) {
-          if (!act[n]) continue;
+          if (!act[n] && !act1[n]) continue;
           f32x4 acc[2];
 #pragma unroll
           for (int qs = 0; qs < 2; ++qs) {
@@ -745,7 +762,7 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
 #pragma unroll
             for (int s = 0; s < KS4; ++s) acc[qs] = mfma16(TL::frag(sq + g * TL::ELEMS, lane, qs, s), kf[n][s], acc[qs]);
           }
-          float ts[2];
+          float ts[2], ts1[2];
           const int base = i0 + 4 * quad - (jw + 16 * n + l16);
 #pragma unroll
           for (int rr = 0; rr < 8; ++rr) {
@@ -753,8 +770,13 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
             const float e = exp2_fast(__builtin_fmaf(acc[rr >> 2][rr & 3], c, nl[rr]));
             const float xv = (inside[n] || (d >= window && d <= hz)) ? e : 0.f;
             ts[rr & 1] = rr < 2 ? xv : ts[rr & 1] + xv;  // the first terms seed the sums
+            if (NB == 2) {
+              const float xv1 = (inside1[n] || (d >= window1 && d <= hz1)) ? e : 0.f;
+              ts1[rr & 1] = rr < 2 ? xv1 : ts1[rr & 1] + xv1;
+            }
           }
-          colsum[g][n] += ts[0] + ts[1];
+          if (act[n]) colsum[g][n] += ts[0] + ts[1];
+          if (NB == 2 && act1[n]) colsum1[g][n] += ts1[0] + ts1[1];
         }
       }
     };
@@ -762,12 +784,12 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     // Exact step (guarded sweep): every admissible pair's exponent x = acc * c -
     // LSE_d log2 e + bias_t log2 e, and per column an online update of (mref, colsum)
     // as in online softmax. A summand of +inf (LSE_d = -inf) makes the mass +inf.
-    auto exact_step = [&](const uint16_t* sq, const float* sl, int i0) __attribute__((always_inline)) {
+    auto exact_step = [&](const uint16_t* sq, const float* sl, int i0, int wb, int hb) __attribute__((always_inline)) {
       bool act[NSUB];
 #pragma unroll
       for (int n = 0; n < NSUB; ++n) {
         const int dlo = i0 - (jw + 16 * n + 15), dhi = i0 + 31 - (jw + 16 * n);
-        act[n] = !(dhi < window || dlo > hz);
+        act[n] = !(dhi < wb || dlo > hb);
       }
 #pragma unroll
       for (int g = 0; g < GC; ++g) {
@@ -790,7 +812,7 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
           for (int rr = 0; rr < 8; ++rr) {
             const int d = base + 16 * (rr >> 2) + (rr & 3);
             const float xr = __builtin_fmaf(acc[rr >> 2][rr & 3], c, nl[rr]) + bl2[n];
-            xv[rr] = (d >= window && d <= hz) ? xr : -__builtin_inff();
+            xv[rr] = (d >= wb && d <= hb) ? xr : -__builtin_inff();
             tmax = fmaxf(tmax, xv[rr]);
           }
           const float mn = fmaxf(mref[g][n], tmax);
@@ -815,10 +837,24 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
       // Differences d = i - j over this wave's keys and the tile's rows.
       const int dmin = i0 - (jw + WK - 1);
       const int dmax = i0 + 31 - jw;
-      if (dmin >= window && dmax <= hz) {
-        full_step(sq, sl);
-      } else if (!(dmax < window || dmin > hz)) {
-        edge_step(sq, sl, i0);
+      if (NB == 1) {
+        if (dmin >= window && dmax <= hz) {
+          full_step(std::integral_constant<int, 1>{}, sq, sl);
+        } else if (!(dmax < window || dmin > hz)) {
+          edge_step(sq, sl, i0);
+        }
+      } else {
+        // Each band is outside this wave's pairs of the step, covers all of them,
+        // or crosses them; any crossing band takes the masked path for both.
+        const bool out0 = dmax < window || dmin > hz, full0 = dmin >= window && dmax <= hz;
+        const bool out1 = dmax < window1 || dmin > hz1, full1 = dmin >= window1 && dmax <= hz1;
+        if ((full0 || out0) && (full1 || out1)) {
+          if (full0 && full1) full_step(std::integral_constant<int, 3>{}, sq, sl);
+          else if (full0) full_step(std::integral_constant<int, 1>{}, sq, sl);
+          else if (full1) full_step(std::integral_constant<int, 2>{}, sq, sl);
+        } else {
+          edge_step(sq, sl, i0);
+        }
       }
       if (more) commit(nsl);
       __syncthreads();
@@ -827,7 +863,10 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
 #pragma unroll
     for (int g = 0; g < GC; ++g)
 #pragma unroll
-      for (int n = 0; n < NSUB; ++n) colsum[g][n] = 0.f;
+      for (int n = 0; n < NSUB; ++n) {
+        colsum[g][n] = 0.f;
+        if (NB == 2) colsum1[g][n] = 0.f;
+      }
     bool bad = false;
     if (!all_exact) {
       issue(0, sq0);
@@ -841,63 +880,72 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
 #pragma unroll
       for (int g = 0; g < GC; ++g)
 #pragma unroll
-        for (int n = 0; n < NSUB; ++n) bad |= !masked[n] && !(colsum[g][n] <= 0.25f * kOverflow);
+        for (int n = 0; n < NSUB; ++n) {
+          bad |= !masked[n] && !(colsum[g][n] <= 0.25f * kOverflow);
+          if (NB == 2) bad |= !masked[n] && !(colsum1[g][n] <= 0.25f * kOverflow);
+        }
     }
 
     // Block-wide: a large bias, or a column sum out of the safe range, takes the
     // chunk through the exact sweep.
     if (all_exact || __syncthreads_or(bad)) {
-      auto xstep = [&](int s, const uint16_t* sq, const float* sl, uint16_t* nsq, float* nsl)
-                       __attribute__((always_inline)) {
-        const bool more = s + 1 < nqt;
-        if (more) issue(s + 1, nsq);
-        const int i0 = (qt_hi - s) * 32;
-        const int dmin = i0 - (jw + WK - 1);
-        const int dmax = i0 + 31 - jw;
-        if (!(dmax < window || dmin > hz)) exact_step(sq, sl, i0);
-        if (more) commit(nsl);
-        __syncthreads();
-      };
+      // One exact sweep per band (over the union of the bands' query tiles).
 #pragma unroll
-      for (int g = 0; g < GC; ++g)
+      for (int bd = 0; bd < NB; ++bd) {
+        const int wb = bd ? window1 : window, hb = bd ? hz1 : hz;
+        float* ob = bd ? out1 : out;
+        auto xstep = [&](int s, const uint16_t* sq, const float* sl, uint16_t* nsq, float* nsl)
+                         __attribute__((always_inline)) {
+          const bool more = s + 1 < nqt;
+          if (more) issue(s + 1, nsq);
+          const int i0 = (qt_hi - s) * 32;
+          const int dmin = i0 - (jw + WK - 1);
+          const int dmax = i0 + 31 - jw;
+          if (!(dmax < wb || dmin > hb)) exact_step(sq, sl, i0, wb, hb);
+          if (more) commit(nsl);
+          __syncthreads();
+        };
 #pragma unroll
-        for (int n = 0; n < NSUB; ++n) {
-          colsum[g][n] = 0.f;
-          mref[g][n] = -__builtin_inff();
-        }
-      issue(0, sq0);
-      commit(sl0);
-      __syncthreads();
-      for (int s = 0; s < nqt; s += 2) {
-        xstep(s, sq0, sl0, sq1, sl1);
-        if (s + 1 < nqt) xstep(s + 1, sq1, sl1, sq0, sl0);
-      }
-      // Merge the four lanes' (mref, sum) pairs of each column and write
-      // exp2(m + log2 sum).
+        for (int g = 0; g < GC; ++g)
 #pragma unroll
-      for (int g = 0; g < GC; ++g) {
-#pragma unroll
-        for (int n = 0; n < NSUB; ++n) {
-          float m = mref[g][n], sm = colsum[g][n];
-#pragma unroll
-          for (int sh = 16; sh <= 32; sh *= 2) {
-            const float mo = __shfl_xor(m, sh);
-            const float so = __shfl_xor(sm, sh);
-            const float mm = fmaxf(m, mo);
-            if (mm == __builtin_inff()) {
-              sm = 1.f;
-            } else if (mm > -__builtin_inff()) {
-              sm = sm * exp2_fast(m - mm) + so * exp2_fast(mo - mm);
-            }
-            m = mm;
+          for (int n = 0; n < NSUB; ++n) {
+            colsum[g][n] = 0.f;
+            mref[g][n] = -__builtin_inff();
           }
-          float v = 0.f;
-          if (m == __builtin_inff()) v = m;
-          else if (m > -__builtin_inff()) v = exp2_fast(m + __log2f(sm));
-          if (masked[n]) v = 0.f;
-          const int j = jw + 16 * n + l16;
-          if (quad == 0 && j < T && (!EPI || out)) out[(head0 + g) * T + j] = v;
-          if (EPI) aggv[n] = agg_mean ? aggv[n] + v : fmaxf(aggv[n], v);
+        issue(0, sq0);
+        commit(sl0);
+        __syncthreads();
+        for (int s = 0; s < nqt; s += 2) {
+          xstep(s, sq0, sl0, sq1, sl1);
+          if (s + 1 < nqt) xstep(s + 1, sq1, sl1, sq0, sl0);
+        }
+        // Merge the four lanes' (mref, sum) pairs of each column and write
+        // exp2(m + log2 sum).
+#pragma unroll
+        for (int g = 0; g < GC; ++g) {
+#pragma unroll
+          for (int n = 0; n < NSUB; ++n) {
+            float m = mref[g][n], sm = colsum[g][n];
+#pragma unroll
+            for (int sh = 16; sh <= 32; sh *= 2) {
+              const float mo = __shfl_xor(m, sh);
+              const float so = __shfl_xor(sm, sh);
+              const float mm = fmaxf(m, mo);
+              if (mm == __builtin_inff()) {
+                sm = 1.f;
+              } else if (mm > -__builtin_inff()) {
+                sm = sm * exp2_fast(m - mm) + so * exp2_fast(mo - mm);
+              }
+              m = mm;
+            }
+            float v = 0.f;
+            if (m == __builtin_inff()) v = m;
+            else if (m > -__builtin_inff()) v = exp2_fast(m + __log2f(sm));
+            if (masked[n]) v = 0.f;
+            const int j = jw + 16 * n + l16;
+            if (quad == 0 && j < T && (!EPI || ob)) ob[(head0 + g) * T + j] = v;
+            if (EPI) aggv[n] = agg_mean ? aggv[n] + v : fmaxf(aggv[n], v);
+          }
         }
       }
     } else {
@@ -912,6 +960,12 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
           const int j = jw + 16 * n + l16;
           if (quad == 0 && j < T && (!EPI || out)) out[(head0 + g) * T + j] = v;
           if (EPI) aggv[n] = agg_mean ? aggv[n] + v : fmaxf(aggv[n], v);
+          if (NB == 2) {
+            float v1 = colsum1[g][n] + __shfl_xor(colsum1[g][n], 16);
+            v1 += __shfl_xor(v1, 32);
+            if (HAS_BIAS) v1 = masked[n] ? 0.f : v1 * fac[n];
+            if (quad == 0 && j < T) out1[(head0 + g) * T + j] = v1;
+          }
         }
       }
     }
@@ -947,13 +1001,14 @@ int launch_p1_d(const Launch& L) {
   return launch_p1_b<D, 1>(L);
 }
 
-template <int D, int NSUB, int GC, bool HB, bool EPI>
+template <int D, int NSUB, int GC, bool HB, bool EPI, int NB>
 int launch_p2(const Launch& L, int hs) {
   constexpr int BK = 4 * NSUB * 16;
   const int nkb = (L.T + BK - 1) / BK;
   const long long grid = (long long)nkb * L.B * L.Hkv;
   const float c = L.scale * kLog2e;
   const int hz = L.horizon < 0 ? L.T : L.horizon;
+  const int hz1 = NB == 2 ? (L.horizon1 < 0 ? L.T : L.horizon1) : 0;
   // Groups an XCD runs at a time: half of its groups when it then still has at
   // least 4 workgroups per slot (2 per CU on its 32 CUs), so that the second half's
   // heaviest blocks start early enough; otherwise all of them.
@@ -963,17 +1018,20 @@ int launch_p2(const Launch& L, int hs) {
     const int ng = nbh / 8;
     xgroups = ng % 2 == 0 && (long long)ng * nkb >= 4 * 64 ? ng / 2 : ng;
   }
-  hipLaunchKernelGGL((future_mass_kernel<D, NSUB, GC, HB, EPI>), dim3((unsigned)(grid * hs)), dim3(256), 0,
+  hipLaunchKernelGGL((future_mass_kernel<D, NSUB, GC, HB, EPI, NB>), dim3((unsigned)(grid * hs)), dim3(256), 0,
                      (hipStream_t)L.stream, reinterpret_cast<const uint16_t*>(L.q),
                      reinterpret_cast<const uint16_t*>(L.k), L.bias, L.lse, L.out, L.B, L.Hq, L.Hkv, L.T, c, L.window,
-                     hz, L.scores, L.agg, L.eps, L.normalize, hs > 1 ? 0 : xgroups, hs);
+                     hz, L.scores, L.agg, L.eps, L.normalize, hs > 1 ? 0 : xgroups, hs, L.window1, hz1, L.out1);
   return (int)hipGetLastError();
 }
 
 template <int D, int NSUB, int GC>
 int launch_p2_b(const Launch& L, int hs) {
-  if (L.scores) return L.bias ? launch_p2<D, NSUB, GC, true, true>(L, 1) : launch_p2<D, NSUB, GC, false, true>(L, 1);
-  return L.bias ? launch_p2<D, NSUB, GC, true, false>(L, hs) : launch_p2<D, NSUB, GC, false, false>(L, hs);
+  if (L.scores)
+    return L.bias ? launch_p2<D, NSUB, GC, true, true, 1>(L, 1) : launch_p2<D, NSUB, GC, false, true, 1>(L, 1);
+  if (L.out1)
+    return L.bias ? launch_p2<D, NSUB, GC, true, false, 2>(L, hs) : launch_p2<D, NSUB, GC, false, false, 2>(L, hs);
+  return L.bias ? launch_p2<D, NSUB, GC, true, false, 1>(L, hs) : launch_p2<D, NSUB, GC, false, false, 1>(L, hs);
 }
 
 template <int D, int NSUB>
@@ -987,7 +1045,8 @@ int launch_p2_gc(const Launch& L) {
   // key in one workgroup). Under 512 workgroups each takes one head, else two.
   // With a short band every block does about the same work and splitting does
   // not pay.
-  const bool long_band = L.horizon < 0 || L.horizon >= L.T / 2;
+  const bool long_band = L.horizon < 0 || L.horizon >= L.T / 2 ||
+                         (L.out1 && (L.horizon1 < 0 || L.horizon1 >= L.T / 2));
   if (!L.scores && grid < 2048 && long_band && G > 1) {
     if (grid >= 512 && G % 2 == 0) return launch_p2_b<D, NSUB, 2>(L, G / 2);
     return launch_p2_b<D, NSUB, 1>(L, G);

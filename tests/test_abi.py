@@ -26,7 +26,8 @@ def test_header_declares_the_entry_points():
     names = set(_declared_functions())
     assert names == {"kvpop_row_lse", "kvpop_future_attn_from_lse", "kvpop_future_attn_target",
                      "kvpop_future_attn_scores", "kvpop_running_topk", "kvpop_running_topk_workspace_size",
-                     "kvpop_sparse_attn_fwd", "kvpop_strerror", "kvpop_abi_version", "kvpop_running_topk_noalloc"}
+                     "kvpop_sparse_attn_fwd", "kvpop_strerror", "kvpop_abi_version", "kvpop_running_topk_noalloc",
+                     "kvpop_future_attn_bands"}
 
 
 def test_library_exports_every_declared_symbol():
@@ -77,7 +78,40 @@ def _sc(d, q=A, k=B_, bias=None, lse=C_, w=0, h=-1, agg=0, eps=1e-8, norm=1, out
                                              eps, norm, out, scores, None)
 
 
+def _bd(d, q=A, k=B_, bias=None, lse=C_, bands=((0, -1), (1, 4096)), outs=(D_, E_), n=None, null=None):
+    n = len(bands) if n is None else n
+    m = max(1, len(bands))
+    w = (ctypes.c_int32 * m)(*[b[0] for b in bands])
+    h = (ctypes.c_int32 * m)(*[b[1] for b in bands])
+    o = (ctypes.c_void_p * max(1, len(outs)))(*outs)
+    args = {"w": w, "h": h, "o": o}
+    if null:
+        args[null] = None
+    return kv.lib().kvpop_future_attn_bands(ctypes.byref(d) if d is not None else None, q, k, bias, lse, n,
+                                            args["w"], args["h"], args["o"], None)
+
+
 EINVAL, EUNS = kv.KVPOP_EINVAL, kv.KVPOP_EUNSUPPORTED
+
+
+def test_bands_argument_checks():
+    """kvpop_future_attn_bands validates like pass 2, per band (fake pointers, nothing launched)."""
+    d = _dims()
+    assert _bd(None) == EINVAL
+    assert _bd(d, n=0) == EINVAL
+    assert _bd(d, n=3) == EINVAL
+    for name in ("w", "h", "o"):
+        assert _bd(d, null=name) == EINVAL, name
+    assert _bd(d, lse=None) == EINVAL
+    assert _bd(d, lse=C_ + 8) == EUNS
+    assert _bd(d, bands=((0, -1), (-1, 5))) == EINVAL
+    assert _bd(d, bands=((3, 2), (1, 5))) == EINVAL
+    assert _bd(d, outs=(D_, D_ + 64)) == EINVAL       # the two outputs overlap
+    assert _bd(d, outs=(D_, C_)) == EINVAL            # an output over the normaliser
+    assert _bd(d, outs=(D_, A + 16)) == EINVAL        # an output over q
+    assert _bd(d, outs=(D_, E_ + 4)) == EUNS
+    assert _bd(d, outs=(None, E_)) == EINVAL
+    assert _bd(_dims(D=96)) == EUNS
 
 
 @pytest.mark.parametrize("call", [_lse, _p2, _tgt, _sc])
@@ -261,7 +295,7 @@ def test_forced_hip_error_path(monkeypatch):
     monkeypatch.setenv("KVPOP_TEST_FORCE_EHIP", str(code))
     d = _dims()
     calls = [lambda: _lse(d), lambda: _p2(d), lambda: _tgt(d), lambda: _sc(d), lambda: _tk(),
-             lambda: _sa(d), lambda: _tkn()]
+             lambda: _sa(d), lambda: _tkn(), lambda: _bd(d)]
     for c in calls:
         assert c() == kv.KVPOP_EHIP
         text = kv.kvpop_strerror(kv.KVPOP_EHIP)

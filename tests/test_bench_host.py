@@ -22,6 +22,15 @@ def test_band_pairs_brute_force(T):
             assert bench.band_pairs(T, window, horizon) == want, (T, window, horizon)
 
 
+@pytest.mark.parametrize("T", [1, 5, 23])
+def test_union_pairs_brute_force(T):
+    bands_list = [[(0, -1)], [(0, -1), (1, 4)], [(2, 3), (5, 9)], [(1, 1), (0, 0)], [(3, -1), (0, 2)], [(1, 6), (4, 9)]]
+    for bands in bands_list:
+        want = sum(1 for d in range(T) for t in range(d + 1)
+                   if any(d - t >= a and (h < 0 or d - t <= h) for a, h in bands))
+        assert bench.union_pairs(T, bands) == want, (T, bands)
+
+
 def test_band_pairs_full_future_is_causal_count():
     assert bench.band_pairs(32768, 0, -1) == 32768 * 32769 // 2
 

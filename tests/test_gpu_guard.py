@@ -6,10 +6,10 @@ sweep and return the mass itself: within the relative 2e-3 bar of the fp64 oracl
 +inf exactly where the mass exceeds the fp32 range, 0 for keys biased -inf, and
 never NaN.
 
-Every case runs three launch forms: kvpop_future_attn_from_lse on a small grid
-(each key block's sweep split over two workgroups), the same on a grid of 2048
-workgroups or more (unsplit), and kvpop_future_attn_scores with its per-head
-masses (the fused epilogue's launch)."""
+The cases run three launch forms: kvpop_future_attn_from_lse on a small grid (the
+query heads of each key block spread over several workgroups), the same on a grid
+of 2048 workgroups or more (every head in one workgroup), and
+kvpop_future_attn_scores with its per-head masses (the fused epilogue's launch)."""
 import math
 
 import numpy as np
@@ -57,7 +57,7 @@ def _check(got, ref, window, what):
 
 
 def _run_all(w, lse, bias, window, horizon):
-    """Masses from the small-grid (split) launch and from the fused-epilogue launch."""
+    """Masses from the small-grid (head-split) launch and from the fused-epilogue launch."""
     q, k = _dev(w.q_bits), _dev(w.k_bits)
     b = _f32(bias) if bias is not None else None
     lse_d = _f32(lse)
@@ -201,3 +201,21 @@ def test_unsplit_launch_with_lowered_normaliser():
         _check(got[b, h][None], ref[None], 0, "unsplit b%d h%d" % (b, h))
     assert np.isposinf(got[3, 5]).sum() > 100
     assert np.isfinite(got[0, 0]).all()
+
+
+def test_two_bands_with_lowered_normaliser():
+    """Both bands of one sweep take the exact path when the normaliser is 80 below
+    the dense one on a few rows, each within the bar of the oracle."""
+    T = 900
+    w = workload.make(_cfg(1, 4, 1, T, 128, seed=507))
+    lse = oracle.row_lse(w.q_bits, w.k_bits, w.scale, w.bias)
+    lse[:, :, [300, 301, 880]] -= 80.0
+    lse32 = lse.astype(np.float32)
+    bands = [(0, -1), (1, 128)]
+    q, k = _dev(w.q_bits), _dev(w.k_bits)
+    outs = kv.kvpop_future_attn_bands(q, k, _f32(lse32), w.scale, bands, key_bias=_f32(w.bias))
+    torch.cuda.synchronize()
+    for (a, h), o in zip(bands, outs):
+        ref = oracle.future_mass(w.q_bits, w.k_bits, w.scale, w.bias, a, h, lse=lse32.astype(np.float64))
+        assert ref.max() > 2.0 ** 64
+        _check(o.cpu().numpy().astype(np.float64), ref, a, "band %s" % ((a, h),))

@@ -102,6 +102,31 @@ def test_shapes_all_bands(shape):
         _check_out(out, ref, window, "shape %s band %s" % (shape, (window, horizon)))
 
 
+BAND_PAIRS = [((0, -1), (1, 1024)), ((1, 1), (0, 5)), ((256, -1), (0, -1)), ((3, 70), (0, 0)), ((1, 40), (1, 40))]
+
+
+@pytest.mark.parametrize("shape", [SHAPES[i] for i in (3, 6, 8, 12, 13, 14)], ids=lambda s: "B%dHq%dHkv%dT%dD%d" % s)
+def test_two_bands_one_sweep(shape):
+    """kvpop_future_attn_bands: both bands from one sweep, each against the oracle,
+    and against kvpop_future_attn_from_lse on that band alone (same terms, up to the
+    fp32 summation order)."""
+    B, Hq, Hkv, T, D = shape
+    w = workload.make(_cfg(B, Hq, Hkv, T, D, seed=T * 3 + Hq, kind="rope", sink=True))
+    q, k = _dev(w.q_bits), _dev(w.k_bits)
+    bias = torch.from_numpy(w.bias).to("cuda")
+    lse = kv.kvpop_row_lse(q, k, w.scale, key_bias=bias)
+    lse_ref = oracle.row_lse(w.q_bits, w.k_bits, w.scale, w.bias)
+    for bands in BAND_PAIRS:
+        outs = kv.kvpop_future_attn_bands(q, k, lse, w.scale, bands, key_bias=bias)
+        singles = [kv.kvpop_future_attn_from_lse(q, k, lse, w.scale, a, h, key_bias=bias) for a, h in bands]
+        torch.cuda.synchronize()
+        for (a, h), o, s1 in zip(bands, outs, singles):
+            got = o.cpu().numpy().astype(np.float64)
+            ref = oracle.future_mass(w.q_bits, w.k_bits, w.scale, w.bias, a, h, lse=lse_ref)
+            _check_out(got, ref, a, "shape %s bands %s band %s" % (shape, bands, (a, h)))
+            np.testing.assert_allclose(got, s1.cpu().numpy(), rtol=1e-5, atol=0)
+
+
 @pytest.mark.parametrize("T", [5, 130, 700])
 def test_random_bias_and_masked_keys(T):
     """Random per-key bias, with every 7th key (from key 1 on) at -inf: masked keys
@@ -328,6 +353,14 @@ def test_long_t128k_as_generated():
             rows = sorted(set(rng.integers(0, w.T, 4).tolist()) | {0, 8191, 8192, w.T - 1})
             np.testing.assert_allclose(lse[0, qh, rows], oracle.row_lse_rows(w.q_bits[0, qh], w.k_bits[0, h], w.scale,
                                                                              rows), atol=LSE_ABS, rtol=0)
+    # both bands from one sweep: the same masses up to the fp32 summation order
+    q, k = _dev(w.q_bits), _dev(w.k_bits)
+    lse_d = torch.from_numpy(lse.astype(np.float32)).to("cuda")
+    fused = kv.kvpop_future_attn_bands(q, k, lse_d, w.scale, w.bands)
+    torch.cuda.synchronize()
+    del q, k, lse_d
+    for o, ref in zip(fused, (full, wband)):
+        np.testing.assert_allclose(o.cpu().numpy(), ref, rtol=2e-5, atol=0)
     for qh, bands in [(5, [0, 1]), (30, [1])]:
         qv, kv_ = w.q_bits[0, qh], w.k_bits[0, qh // w.G]
         lse_ref = oracle.row_lse_blocked(qv, kv_, w.scale, block=512, threads=THREADS)
