@@ -631,8 +631,13 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     // never wait for each other. Values run key-subtile fastest, so consecutive
     // adds go to different partial sums.
     // BANDS: bit b set = band b takes this step's sums (always 1 with one band).
-    auto full_step = [&](auto bands_c, const uint16_t* sq, const float* sl) __attribute__((always_inline)) {
+    // MASKED (a band edge, one band, two key subtiles per wave): the accumulators
+    // start from minit, 0 on the band's pairs and -inf elsewhere, so pairs outside
+    // the band add exp2(-inf) = 0 and the step keeps the pipelined form.
+    auto full_step = [&](auto bands_c, auto masked_c, const f32x4 (&minit)[2][NSUB], const uint16_t* sq,
+                         const float* sl) __attribute__((always_inline)) {
       constexpr int BANDS = decltype(bands_c)::value;
+      constexpr bool MASKED = decltype(masked_c)::value;
       bf16x8 fr[2][KS4];
       float nl[2][8];
       f32x4 acc_prev[2][NSUB];
@@ -649,7 +654,7 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
 #pragma unroll
         for (int qs = 0; qs < 2; ++qs)
 #pragma unroll
-          for (int n = 0; n < NSUB; ++n) acc[qs][n] = f32x4{};
+          for (int n = 0; n < NSUB; ++n) acc[qs][n] = MASKED ? minit[qs][n] : f32x4{};
         float ts[NSUB];
         float y[NV], x[NV];
         const float(&pnl)[8] = nl[(g + 1) & 1];  // head g - 1's normalisers
@@ -800,6 +805,7 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
       }
     };
 
+    const f32x4 zinit[2][NSUB] = {};  // (unused by the unmasked steps)
     auto step = [&](int s, const uint16_t* sq, const float* sl, uint16_t* nsq, float* nsl) __attribute__((always_inline)) {
       const bool more = s + 1 < nqt;
       if (more) issue(s + 1, nsq);
@@ -809,9 +815,23 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
       const int dmax = i0 + 31 - jw;
       if (NB == 1) {
         if (dmin >= window && dmax <= hz) {
-          full_step(std::integral_constant<int, 1>{}, sq, sl);
+          full_step(std::integral_constant<int, 1>{}, std::false_type{}, zinit, sq, sl);
         } else if (!(dmax < window || dmin > hz)) {
-          edge_step(sq, sl, i0);
+          if (NSUB == 2) {
+            f32x4 minit[2][NSUB];
+#pragma unroll
+            for (int qs = 0; qs < 2; ++qs)
+#pragma unroll
+              for (int n = 0; n < NSUB; ++n)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                  const int d = i0 + 16 * qs + 4 * quad + r - (jw + 16 * n + l16);
+                  minit[qs][n][r] = (d >= window && d <= hz) ? 0.f : -__builtin_inff();
+                }
+            full_step(std::integral_constant<int, 1>{}, std::true_type{}, minit, sq, sl);
+          } else {
+            edge_step(sq, sl, i0);
+          }
         }
       } else {
         // Each band is outside this wave's pairs of the step, covers all of them,
@@ -819,9 +839,9 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
         const bool out0 = dmax < window || dmin > hz, full0 = dmin >= window && dmax <= hz;
         const bool out1 = dmax < window1 || dmin > hz1, full1 = dmin >= window1 && dmax <= hz1;
         if ((full0 || out0) && (full1 || out1)) {
-          if (full0 && full1) full_step(std::integral_constant<int, 3>{}, sq, sl);
-          else if (full0) full_step(std::integral_constant<int, 1>{}, sq, sl);
-          else if (full1) full_step(std::integral_constant<int, 2>{}, sq, sl);
+          if (full0 && full1) full_step(std::integral_constant<int, 3>{}, std::false_type{}, zinit, sq, sl);
+          else if (full0) full_step(std::integral_constant<int, 1>{}, std::false_type{}, zinit, sq, sl);
+          else if (full1) full_step(std::integral_constant<int, 2>{}, std::false_type{}, zinit, sq, sl);
         } else {
           edge_step(sq, sl, i0);
         }
@@ -1031,8 +1051,11 @@ template <int D>
 int launch_p2_d(const Launch& L) {
   // Four 16-key subtiles per wave (256 keys per workgroup) unless that leaves fewer
   // than ~2 workgroups per CU; then two (128 keys).
+  // A short single band (horizon under T / 2) also takes two: its band edges are a
+  // large share of the steps, and with two subtiles they keep the pipelined form.
   const long long wg2 = (long long)L.B * L.Hkv * ((L.T + 255) / 256);
-  if (wg2 >= 512) return launch_p2_gc<D, 4>(L);
+  const bool short_band = L.horizon >= 0 && L.horizon < L.T / 2 && !L.out1;
+  if (wg2 >= 512 && !short_band) return launch_p2_gc<D, 4>(L);
   return launch_p2_gc<D, 2>(L);
 }
 
