@@ -43,6 +43,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
 #include <type_traits>
 
 
@@ -118,8 +119,8 @@ struct Tile16 {
 // Pass 1: row log-normaliser.
 //
 // Workgroup = (batch b, KV head h, head chunk pc of P query heads, query block of
-// BQ = 256 / P positions). Its 4 waves x NQ = 4 column subtiles of 16 (head,
-// query) columns keep their Q rows in registers as the B operand of
+// BQ = 64 NQ / P positions). Its 4 waves x NQ column subtiles of 16 (head, query)
+// columns keep their Q rows in registers as the B operand of
 // v_mfma_f32_16x16x32_bf16. One step streams KT = 4 key tiles of 32 rows through
 // LDS (wave w copies tile w), shared by all P heads. A lane holds, per key tile, 8
 // key rows (2 key subtiles x 4) of each of its NQ query columns.
@@ -135,15 +136,17 @@ struct Tile16 {
 // bound; a sum that gets there from smaller terms only costs a redo. The result is
 // the same LSE; the common path costs one fma, one exp and one add per pair.
 // ---------------------------------------------------------------------------
-template <int D, int P, bool HAS_BIAS>
+template <int D, int P, bool HAS_BIAS, int NQ>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2))) void
 row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const float* __restrict__ bias,
-               float* __restrict__ lse, int B, int Hq, int Hkv, int T, float c, float inv_scale, int nqb, int xg) {
-  constexpr int NQ = 4;   // 16-query column subtiles per wave
+               float* __restrict__ lse, int B, int Hq, int Hkv, int T, float c, float inv_scale, int nqb, int xg,
+               int zh) {
+  static_assert(NQ == 2 || NQ == 4, "16-query column subtiles per wave");
   constexpr int KT = 4;   // 32-key tiles per step
   using TL = Tile16<D>;
   constexpr int KS4 = TL::KS4;
-  constexpr int SPH = 16 / P;  // column subtiles per head
+  constexpr int SPH = 4 * NQ / P;  // column subtiles per head
+  static_assert(SPH >= 1, "at least one subtile per head");
   constexpr int BQ = 16 * SPH;
   constexpr int NV = 2 * 4 * NQ;        // values per lane and key tile
   constexpr int SLOTS = 2 * KS4 * NQ;   // MFMAs per key tile
@@ -163,7 +166,10 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
   // 8 XCDs round-robin (XCD = blockIdx % 8). With xg > 0 (per a multiple of 8) XCD x
   // owns the (b, KV head, head chunk) groups x, x + 8, ... and runs them xg at a
   // time, so that fewer groups share its L2; otherwise the order is query block
-  // major over all groups.
+  // major over all groups. With zh > 0 (a grid of zh to 2 zh workgroups, zh the
+  // number of CUs) every workgroup starts at once, and the dispatcher gives workgroup
+  // i + zh the CU of workgroup i: the second zh take the blocks lightest first, so
+  // that each CU pairs a heavy block with a light one.
   int order, rest;
   if (xg > 0) {
     const int x = (int)(blockIdx.x & 7), j = (int)(blockIdx.x >> 3);
@@ -171,6 +177,10 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
     const int batch = j / span, r = j - batch * span;
     order = r / xg;
     rest = x + 8 * (batch * xg + r - order * xg);
+  } else if (zh > 0 && (int)blockIdx.x >= zh) {
+    const int j = (int)blockIdx.x - zh;
+    order = nqb - 1 - j / per;
+    rest = j - (j / per) * per;
   } else {
     order = blockIdx.x / per;
     rest = blockIdx.x - order * per;
@@ -437,7 +447,10 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
 //
 // Query rows beyond T get LSE = +inf in LDS, which zeroes their terms. A per-key
 // bias is factored out of the sum, out_t = exp(bias_t) * sum_d exp(...). Query
-// heads are processed GC at a time; G / GC chunks each repeat the sweep.
+// heads are processed GC at a time; G / GC chunks each repeat the sweep. With one
+// head at a time (GC = 1) a step stages two consecutive query tiles of it, so the
+// sweep takes half as many steps: on small grids the heaviest key block's chain of
+// steps sets the time, and each step pays a barrier and the load latency.
 //
 // Guard. The fast sweep sums exp2(x) against the fixed reference 0, which is safe
 // when every summand is a probability (the dense normaliser) and the factored bias
@@ -470,16 +483,21 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
   constexpr int KS4 = TL::KS4;
   constexpr int WK = NSUB * 16;  // keys per wave
   constexpr int BK = 4 * WK;     // keys per workgroup
-  constexpr int PPW = GC * TL::PLANES / 4;  // LDS planes each wave copies per step
+  // A step stages U = GC * TPS query tiles ("units"): TPS consecutive tiles of each
+  // of GC heads. One head per step (GC = 1) takes two tiles, so that a sweep has
+  // half as many steps (each step's barrier and load latency paid half as often).
+  constexpr int TPS = GC == 1 ? 2 : 1;
+  constexpr int U = GC * TPS;
+  constexpr int PPW = U * TL::PLANES / 4;  // LDS planes each wave copies per step
   static_assert(PPW >= 1 && TL::PLANES % PPW == 0, "plane split");
-  constexpr int NV = 8 * NSUB;              // values per lane, head and step
-  constexpr int SLOTS = 2 * KS4 * NSUB;     // MFMAs per head and step
+  constexpr int NV = 8 * NSUB;              // values per lane, unit and step
+  constexpr int SLOTS = 2 * KS4 * NSUB;     // MFMAs per unit and step
   constexpr int V = NV / SLOTS;             // values per MFMA slot
   static_assert(V * SLOTS == NV, "values per slot");
-  __shared__ __attribute__((aligned(16))) uint16_t sq0[GC * TL::ELEMS];
-  __shared__ __attribute__((aligned(16))) uint16_t sq1[GC * TL::ELEMS];
-  __shared__ __attribute__((aligned(16))) float sl0[GC * 32];
-  __shared__ __attribute__((aligned(16))) float sl1[GC * 32];
+  __shared__ __attribute__((aligned(16))) uint16_t sq0[U * TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) uint16_t sq1[U * TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) float sl0[U * 32];
+  __shared__ __attribute__((aligned(16))) float sl1[U * 32];
 
   const int tid = threadIdx.x, lane = tid & 63, quad = lane >> 4, l16 = lane & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, uniform per wave
@@ -528,6 +546,7 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     qt_hi = (int)(r_hi / 32);
     nqt = qt_hi - (int)(r_lo / 32) + 1;
   }
+  const int nst = (nqt + TPS - 1) / TPS;  // steps; step s covers tiles qt_hi - TPS s - t, t < TPS
 
   // Bias of this lane's key columns: factored out (fac) by the fast sweep, added to
   // every exponent (bl2, log2 units) by the exact sweep. masked: bias -inf.
@@ -598,24 +617,28 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
   }
 
   const int voff0 = TL::lane_voffset(lane, 0), voff1 = TL::lane_voffset(lane, 1);
-  const int pg = (w * PPW) / TL::PLANES;          // the head tile this wave copies
+  const int pg = (w * PPW) / TL::PLANES;          // the unit (tile) this wave copies
   const int pp0 = (w * PPW) - pg * TL::PLANES;    // its first plane
 
   for (int gh0 = h * G + ch * GC; gh0 < (h + 1) * G; gh0 += GC * hs) {
     const size_t head0 = (size_t)(b * Hq + gh0);
     float stl = 0.f;
     // Start the loads of step s: Q tiles straight into LDS, raw LSE into a register.
+    // Unit u of step s: head head0 + u / TPS, rows from (qt_hi - TPS s - u % TPS) * 32.
+    // A tile below row 0 (the last step of a sweep with an odd tile count) loads
+    // nothing (zero rows) and gets LSE = +inf, which zeroes its terms.
     auto issue = [&](int s, uint16_t* sq) __attribute__((always_inline)) {
-      const int i0 = (qt_hi - s) * 32;
-      TL::template planes_to_lds<PPW>(sq + pg * TL::ELEMS, Q + ((head0 + pg) * T + i0) * D, min(32, T - i0), pp0,
-                                      voff0, voff1);
-      if (tid < GC * 32) {
-        const int i = i0 + (tid & 31);
-        stl = i < T ? lse[(head0 + (tid >> 5)) * T + i] : __builtin_inff();
+      const int ti = (qt_hi - TPS * s - pg % TPS) * 32;
+      TL::template planes_to_lds<PPW>(sq + pg * TL::ELEMS, Q + ((head0 + pg / TPS) * T + max(ti, 0)) * D,
+                                      ti < 0 ? 0 : min(32, T - ti), pp0, voff0, voff1);
+      if (tid < U * 32) {
+        const int u = tid >> 5;
+        const int i = (qt_hi - TPS * s - u % TPS) * 32 + (tid & 31);
+        stl = i >= 0 && i < T ? lse[(head0 + u / TPS) * T + i] : __builtin_inff();
       }
     };
     auto commit = [&](float* sl) __attribute__((always_inline)) {
-      if (tid < GC * 32) sl[tid] = -stl * kLog2e;
+      if (tid < U * 32) sl[tid] = -stl * kLog2e;
     };
 
     float colsum[GC][NSUB];  // fast sweep: column sums; exact sweep: sums relative to mref
@@ -634,22 +657,22 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
       }
     };
 
-    // Fully admissible step, as a software pipeline over the GC heads with a fixed
+    // Fully admissible step, as a software pipeline over the U units with a fixed
     // issue order (the scheduling barriers stop the compiler from regrouping it).
-    // Head g's unit runs its 2 NSUB MFMA chains k-step by k-step, so each A fragment
-    // read from LDS feeds NSUB MFMAs; right after those the fragment register is
-    // refilled with head g + 1's operand (used a whole unit later, hiding the LDS
-    // latency). Each MFMA slot also issues the VALU work of head g - 1's values,
-    // itself pipelined over three slots: the fma of value v, the exp of value v - V
-    // and the add of value v - 2 V, so that the three instructions after one MFMA
-    // never wait for each other. Values run key-subtile fastest, so consecutive
-    // adds go to different partial sums.
+    // Unit g runs its 2 NSUB MFMA chains k-step by k-step, so each A fragment read
+    // from LDS feeds NSUB MFMAs; right after those the fragment register is refilled
+    // with unit g + 1's operand (used a whole unit later, hiding the LDS latency).
+    // Each MFMA slot also issues the VALU work of unit g - 1's values, itself
+    // pipelined over three slots: the fma of value v, the exp of value v - V and the
+    // add of value v - 2 V, so that the three instructions after one MFMA never wait
+    // for each other. Values run key-subtile fastest, so consecutive adds go to
+    // different partial sums. i0: the step's first (highest) tile.
     // BANDS: bit b set = band b takes this step's sums (always 1 with one band).
-    // MASKED (a band edge, one band, two key subtiles per wave): the accumulators
-    // start from minit, 0 on the band's pairs and -inf elsewhere, so pairs outside
-    // the band add exp2(-inf) = 0 and the step keeps the pipelined form.
-    auto full_step = [&](auto bands_c, auto masked_c, const f32x4 (&minit)[2][NSUB], const uint16_t* sq,
-                         const float* sl) __attribute__((always_inline)) {
+    // MASKED (a band edge, one band, two key subtiles per wave): each unit's
+    // accumulators start at 0 on the band's pairs and -inf elsewhere, so pairs
+    // outside the band add exp2(-inf) = 0 and the step keeps the pipelined form.
+    auto full_step = [&](auto bands_c, auto masked_c, int i0, const uint16_t* sq, const float* sl)
+                         __attribute__((always_inline)) {
       constexpr int BANDS = decltype(bands_c)::value;
       constexpr bool MASKED = decltype(masked_c)::value;
       bf16x8 fr[2][KS4];
@@ -662,16 +685,25 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
       read_nl(sl, 0, nl[0]);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int g = 0; g <= GC; ++g) {
-        if (g > 0 && g < GC) read_nl(sl, g, nl[g & 1]);
+      for (int g = 0; g <= U; ++g) {
+        if (g > 0 && g < U) read_nl(sl, g, nl[g & 1]);
         f32x4 acc[2][NSUB];
 #pragma unroll
         for (int qs = 0; qs < 2; ++qs)
 #pragma unroll
-          for (int n = 0; n < NSUB; ++n) acc[qs][n] = MASKED ? minit[qs][n] : f32x4{};
+          for (int n = 0; n < NSUB; ++n) {
+            acc[qs][n] = f32x4{};
+            if (MASKED && g < U) {
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                const int d = i0 - 32 * (g % TPS) + 16 * qs + 4 * quad + r - (jw + 16 * n + l16);
+                acc[qs][n][r] = (d >= window && d <= hz) ? 0.f : -__builtin_inff();
+              }
+            }
+          }
         float ts[NSUB];
         float y[NV], x[NV];
-        const float(&pnl)[8] = nl[(g + 1) & 1];  // head g - 1's normalisers
+        const float(&pnl)[8] = nl[(g + 1) & 1];  // unit g - 1's normalisers
         // value v of head g - 1: key subtile v % NSUB, row slot v / NSUB = 4 qs + r
         auto val = [&](int v) __attribute__((always_inline)) {
           const int n = v % NSUB, rr = v / NSUB;
@@ -688,9 +720,9 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
           for (int qs = 0; qs < 2; ++qs) {
 #pragma unroll
             for (int n = 0; n < NSUB; ++n) {
-              if (g < GC) {
+              if (g < U) {
                 acc[qs][n] = mfma16(fr[qs][s], kf[n][s], acc[qs][n]);
-                if (n == NSUB - 1 && g + 1 < GC) fr[qs][s] = TL::frag(sq + (g + 1) * TL::ELEMS, lane, qs, s);
+                if (n == NSUB - 1 && g + 1 < U) fr[qs][s] = TL::frag(sq + (g + 1) * TL::ELEMS, lane, qs, s);
               }
               if (g > 0) {
 #pragma unroll
@@ -713,8 +745,8 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
           for (int v = NV - 2 * V; v < NV; ++v) add(v);
 #pragma unroll
           for (int n = 0; n < NSUB; ++n) {
-            if (BANDS & 1) colsum[g - 1][n] += ts[n];
-            if (BANDS & 2) colsum1[g - 1][n] += ts[n];
+            if (BANDS & 1) colsum[(g - 1) / TPS][n] += ts[n];
+            if (BANDS & 2) colsum1[(g - 1) / TPS][n] += ts[n];
           }
         }
 #pragma unroll
@@ -728,17 +760,18 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     // the band (skipped), inside it (summed without a mask) or across its edge (each
     // pair masked by window <= i - j <= hz).
     auto edge_step = [&](const uint16_t* sq, const float* sl, int i0) __attribute__((always_inline)) {
-      bool act[NSUB], inside[NSUB], act1[NSUB], inside1[NSUB];
 #pragma unroll
-      for (int n = 0; n < NSUB; ++n) {
-        const int dlo = i0 - (jw + 16 * n + 15), dhi = i0 + 31 - (jw + 16 * n);
-        act[n] = !(dhi < window || dlo > hz);
-        inside[n] = dlo >= window && dhi <= hz;
-        act1[n] = NB == 2 && !(dhi < window1 || dlo > hz1);
-        inside1[n] = NB == 2 && dlo >= window1 && dhi <= hz1;
-      }
+      for (int g = 0; g < U; ++g) {
+        const int iu = i0 - 32 * (g % TPS);
+        bool act[NSUB], inside[NSUB], act1[NSUB], inside1[NSUB];
 #pragma unroll
-      for (int g = 0; g < GC; ++g) {
+        for (int n = 0; n < NSUB; ++n) {
+          const int dlo = iu - (jw + 16 * n + 15), dhi = iu + 31 - (jw + 16 * n);
+          act[n] = !(dhi < window || dlo > hz);
+          inside[n] = dlo >= window && dhi <= hz;
+          act1[n] = NB == 2 && !(dhi < window1 || dlo > hz1);
+          inside1[n] = NB == 2 && dlo >= window1 && dhi <= hz1;
+        }
         float nl[8];
         read_nl(sl, g, nl);
 #pragma unroll
@@ -752,7 +785,7 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
             for (int s = 0; s < KS4; ++s) acc[qs] = mfma16(TL::frag(sq + g * TL::ELEMS, lane, qs, s), kf[n][s], acc[qs]);
           }
           float ts[2], ts1[2];
-          const int base = i0 + 4 * quad - (jw + 16 * n + l16);
+          const int base = iu + 4 * quad - (jw + 16 * n + l16);
 #pragma unroll
           for (int rr = 0; rr < 8; ++rr) {
             const int d = base + 16 * (rr >> 2) + (rr & 3);
@@ -764,8 +797,8 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
               ts1[rr & 1] = rr < 2 ? xv1 : ts1[rr & 1] + xv1;
             }
           }
-          if (act[n]) colsum[g][n] += ts[0] + ts[1];
-          if (NB == 2 && act1[n]) colsum1[g][n] += ts1[0] + ts1[1];
+          if (act[n]) colsum[g / TPS][n] += ts[0] + ts[1];
+          if (NB == 2 && act1[n]) colsum1[g / TPS][n] += ts1[0] + ts1[1];
         }
       }
     };
@@ -774,14 +807,15 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     // LSE_d log2 e + bias_t log2 e, and per column an online update of (mref, colsum)
     // as in online softmax. A summand of +inf (LSE_d = -inf) makes the mass +inf.
     auto exact_step = [&](const uint16_t* sq, const float* sl, int i0, int wb, int hb) __attribute__((always_inline)) {
-      bool act[NSUB];
 #pragma unroll
-      for (int n = 0; n < NSUB; ++n) {
-        const int dlo = i0 - (jw + 16 * n + 15), dhi = i0 + 31 - (jw + 16 * n);
-        act[n] = !(dhi < wb || dlo > hb);
-      }
+      for (int g = 0; g < U; ++g) {
+        const int iu = i0 - 32 * (g % TPS), gh = g / TPS;
+        bool act[NSUB];
 #pragma unroll
-      for (int g = 0; g < GC; ++g) {
+        for (int n = 0; n < NSUB; ++n) {
+          const int dlo = iu - (jw + 16 * n + 15), dhi = iu + 31 - (jw + 16 * n);
+          act[n] = !(dhi < wb || dlo > hb);
+        }
         float nl[8];
         read_nl(sl, g, nl);
 #pragma unroll
@@ -794,7 +828,7 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
 #pragma unroll
             for (int s = 0; s < KS4; ++s) acc[qs] = mfma16(TL::frag(sq + g * TL::ELEMS, lane, qs, s), kf[n][s], acc[qs]);
           }
-          const int base = i0 + 4 * quad - (jw + 16 * n + l16);
+          const int base = iu + 4 * quad - (jw + 16 * n + l16);
           float xv[8];
           float tmax = -__builtin_inff();
 #pragma unroll
@@ -804,48 +838,34 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
             xv[rr] = (d >= wb && d <= hb) ? xr : -__builtin_inff();
             tmax = fmaxf(tmax, xv[rr]);
           }
-          const float mn = fmaxf(mref[g][n], tmax);
+          const float mn = fmaxf(mref[gh][n], tmax);
           if (mn == __builtin_inff()) {
-            mref[g][n] = mn;
-            colsum[g][n] = 1.f;
+            mref[gh][n] = mn;
+            colsum[gh][n] = 1.f;
           } else if (mn > -__builtin_inff()) {
             float e = 0.f;
 #pragma unroll
             for (int rr = 0; rr < 8; ++rr) e += exp2_fast(xv[rr] - mn);
-            colsum[g][n] = colsum[g][n] * exp2_fast(mref[g][n] - mn) + e;
-            mref[g][n] = mn;
+            colsum[gh][n] = colsum[gh][n] * exp2_fast(mref[gh][n] - mn) + e;
+            mref[gh][n] = mn;
           }
         }
       }
     };
 
-    const f32x4 zinit[2][NSUB] = {};  // (unused by the unmasked steps)
     auto step = [&](int s, const uint16_t* sq, const float* sl, uint16_t* nsq, float* nsl) __attribute__((always_inline)) {
-      const bool more = s + 1 < nqt;
+      const bool more = s + 1 < nst;
       if (more) issue(s + 1, nsq);
-      const int i0 = (qt_hi - s) * 32;
-      // Differences d = i - j over this wave's keys and the tile's rows.
-      const int dmin = i0 - (jw + WK - 1);
+      const int i0 = (qt_hi - TPS * s) * 32;
+      // Differences d = i - j over this wave's keys and the step's rows.
+      const int dmin = i0 - 32 * (TPS - 1) - (jw + WK - 1);
       const int dmax = i0 + 31 - jw;
       if (NB == 1) {
         if (dmin >= window && dmax <= hz) {
-          full_step(std::integral_constant<int, 1>{}, std::false_type{}, zinit, sq, sl);
+          full_step(std::integral_constant<int, 1>{}, std::false_type{}, i0, sq, sl);
         } else if (!(dmax < window || dmin > hz)) {
-          if (NSUB == 2) {
-            f32x4 minit[2][NSUB];
-#pragma unroll
-            for (int qs = 0; qs < 2; ++qs)
-#pragma unroll
-              for (int n = 0; n < NSUB; ++n)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                  const int d = i0 + 16 * qs + 4 * quad + r - (jw + 16 * n + l16);
-                  minit[qs][n][r] = (d >= window && d <= hz) ? 0.f : -__builtin_inff();
-                }
-            full_step(std::integral_constant<int, 1>{}, std::true_type{}, minit, sq, sl);
-          } else {
-            edge_step(sq, sl, i0);
-          }
+          if (NSUB == 2) full_step(std::integral_constant<int, 1>{}, std::true_type{}, i0, sq, sl);
+          else edge_step(sq, sl, i0);
         }
       } else {
         // Each band is outside this wave's pairs of the step, covers all of them,
@@ -853,9 +873,9 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
         const bool out0 = dmax < window || dmin > hz, full0 = dmin >= window && dmax <= hz;
         const bool out1 = dmax < window1 || dmin > hz1, full1 = dmin >= window1 && dmax <= hz1;
         if ((full0 || out0) && (full1 || out1)) {
-          if (full0 && full1) full_step(std::integral_constant<int, 3>{}, std::false_type{}, zinit, sq, sl);
-          else if (full0) full_step(std::integral_constant<int, 1>{}, std::false_type{}, zinit, sq, sl);
-          else if (full1) full_step(std::integral_constant<int, 2>{}, std::false_type{}, zinit, sq, sl);
+          if (full0 && full1) full_step(std::integral_constant<int, 3>{}, std::false_type{}, i0, sq, sl);
+          else if (full0) full_step(std::integral_constant<int, 1>{}, std::false_type{}, i0, sq, sl);
+          else if (full1) full_step(std::integral_constant<int, 2>{}, std::false_type{}, i0, sq, sl);
         } else {
           edge_step(sq, sl, i0);
         }
@@ -876,9 +896,9 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
       issue(0, sq0);
       commit(sl0);
       __syncthreads();
-      for (int s = 0; s < nqt; s += 2) {
+      for (int s = 0; s < nst; s += 2) {
         step(s, sq0, sl0, sq1, sl1);
-        if (s + 1 < nqt) step(s + 1, sq1, sl1, sq0, sl0);
+        if (s + 1 < nst) step(s + 1, sq1, sl1, sq0, sl0);
       }
       // Each of the four lane sums at most 2^62 keeps the column's sum within 2^64.
 #pragma unroll
@@ -900,10 +920,10 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
         float* ob = bd ? out1 : out;
         auto xstep = [&](int s, const uint16_t* sq, const float* sl, uint16_t* nsq, float* nsl)
                          __attribute__((always_inline)) {
-          const bool more = s + 1 < nqt;
+          const bool more = s + 1 < nst;
           if (more) issue(s + 1, nsq);
-          const int i0 = (qt_hi - s) * 32;
-          const int dmin = i0 - (jw + WK - 1);
+          const int i0 = (qt_hi - TPS * s) * 32;
+          const int dmin = i0 - 32 * (TPS - 1) - (jw + WK - 1);
           const int dmax = i0 + 31 - jw;
           if (!(dmax < wb || dmin > hb)) exact_step(sq, sl, i0, wb, hb);
           if (more) commit(nsl);
@@ -919,9 +939,9 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
         issue(0, sq0);
         commit(sl0);
         __syncthreads();
-        for (int s = 0; s < nqt; s += 2) {
+        for (int s = 0; s < nst; s += 2) {
           xstep(s, sq0, sl0, sq1, sl1);
-          if (s + 1 < nqt) xstep(s + 1, sq1, sl1, sq0, sl0);
+          if (s + 1 < nst) xstep(s + 1, sq1, sl1, sq0, sl0);
         }
         // Merge the four lanes' (mref, sum) pairs of each column and write
         // exp2(m + log2 sum).
@@ -977,9 +997,24 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
   if (EPI) write_scores();
 }
 
-template <int D, int P, bool HB>
-int launch_p1(const Launch& L) {
-  constexpr int BQ = 256 / P;
+// Compute units of the stream's device, looked up once per device.
+int stream_cus(void* stream) {
+  constexpr int kDevices = 64;
+  static std::atomic<int> cache[kDevices];
+  int dev = 0;
+  if (hipStreamGetDevice((hipStream_t)stream, &dev) != hipSuccess && hipGetDevice(&dev) != hipSuccess) return 0;
+  if (dev < 0 || dev >= kDevices) return 0;
+  int n = cache[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return 0;
+    cache[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
+
+template <int D, int P, bool HB, int NQ>
+int launch_p1_q(const Launch& L) {
+  constexpr int BQ = 64 * NQ / P;
   const int G = L.Hq / L.Hkv;
   const int nqb = (L.T + BQ - 1) / BQ;
   const long long per = (long long)L.B * L.Hkv * (G / P);
@@ -989,10 +1024,30 @@ int launch_p1(const Launch& L) {
   // 32768 at P = 4): at B = 4, T = 32768 pass 1 then fetches 3.2 instead of 9.8 GB
   // from HBM per launch and holds a 2% higher clock.
   const int xg = per % 8 == 0 && nqb >= 512 ? 1 : 0;
-  hipLaunchKernelGGL((row_lse_kernel<D, P, HB>), dim3((unsigned)grid), dim3(256), 0, (hipStream_t)L.stream,
+  // A grid that the CUs hold at once (two workgroups each) pairs heavy and light
+  // blocks on each CU. At B = 1, T = 4096 (512 workgroups) the heaviest CU then has
+  // about 33 key steps instead of 48.
+  const int ncu = stream_cus(L.stream);
+  const int zh = xg == 0 && grid > ncu && grid <= 2LL * ncu && ncu % per == 0 ? ncu : 0;
+  hipLaunchKernelGGL((row_lse_kernel<D, P, HB, NQ>), dim3((unsigned)grid), dim3(256), 0, (hipStream_t)L.stream,
                      reinterpret_cast<const uint16_t*>(L.q), reinterpret_cast<const uint16_t*>(L.k), L.bias, L.out,
-                     L.B, L.Hq, L.Hkv, L.T, c, 1.0f / L.scale, nqb, xg);
+                     L.B, L.Hq, L.Hkv, L.T, c, 1.0f / L.scale, nqb, xg, zh);
   return (int)hipGetLastError();
+}
+
+// A grid of full-height blocks (NQ = 4) that fits on the CUs one workgroup each
+// takes half-height blocks instead (NQ = 2; P = 8 keeps 4): twice the workgroups,
+// and the heaviest block, whose sweep sets the time when every workgroup starts at
+// once, has half the work (B = 1, T = 2048: 0.042 -> 0.031 ms). With more blocks
+// the full-height form is faster (B = 1, T = 4096: 0.090 against 0.097 ms).
+template <int D, int P, bool HB>
+int launch_p1(const Launch& L) {
+  const int G = L.Hq / L.Hkv;
+  const long long grid4 = (long long)((L.T + 256 / P - 1) / (256 / P)) * L.B * L.Hkv * (G / P);
+  if constexpr (P < 8) {
+    if (grid4 <= stream_cus(L.stream)) return launch_p1_q<D, P, HB, 2>(L);
+  }
+  return launch_p1_q<D, P, HB, 4>(L);
 }
 
 template <int D, int P>

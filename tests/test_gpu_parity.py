@@ -171,6 +171,37 @@ def test_logits_far_above_the_diagonal_reference(T, D):
         _check_out(out, ref, window, "large bias band %s" % ((window, horizon),))
 
 
+@pytest.mark.parametrize("shape", [(1, 32, 8, 2048), (1, 32, 8, 4096), (8, 8, 2, 4100), (9, 8, 2, 4100)],
+                         ids=lambda s: "B%dHq%dHkv%dT%d" % s)
+def test_pass1_block_forms(shape):
+    """Pass 1 has four launch forms, by grid size (P = 4 query heads per workgroup,
+    blocks of 64 NQ / P queries, 256 CUs):
+      B=1, 32/8, T=2048: 256 full-height blocks fit on the CUs one each, so NQ = 2
+        (512 half-height blocks), and the grid holds two per CU: heavy and light
+        blocks paired on each CU;
+      B=1, 32/8, T=4096: NQ = 4, 512 blocks, paired;
+      B=8, 8/2, T=4100: NQ = 4, 1040 blocks, heaviest first;
+      B=9, 8/2, T=4100: NQ = 4, 1170 blocks, heaviest first, a grid that is not a
+        multiple of the workgroups per CU.
+    Key 0 carries a bias of +60 and keys T/2 .. T/2+4 one of +45, so every form
+    also takes the exact redo of off-diagonal steps. Every LSE row of eight query
+    heads (all KV heads, first and last batch row) must match the oracle."""
+    B, Hq, Hkv, T = shape
+    D = 128
+    w = workload.make(_cfg(B, Hq, Hkv, T, D, seed=900 + B + T))
+    bias = np.zeros(T, np.float32)
+    bias[0] = 60.0
+    bias[T // 2:T // 2 + 5] = 45.0
+    q, k = _dev(w.q_bits), _dev(w.k_bits)
+    bd = torch.from_numpy(bias).to("cuda")
+    lse = kv.kvpop_row_lse(q, k, w.scale, key_bias=bd).cpu().numpy().astype(np.float64)
+    heads = sorted({(b, qh) for b in (0, B - 1) for qh in range(0, Hq, max(1, Hq // 4))} | {(B - 1, Hq - 1)})
+    for b, qh in heads:
+        ref = oracle.row_lse_blocked(w.q_bits[b, qh], w.k_bits[b, qh // w.G], w.scale, bias, block=512,
+                                     threads=THREADS)
+        _check_lse(lse[b, qh], ref, "b%d qh%d" % (b, qh))
+
+
 def test_tiny_config():
     """T=512, one head, D=64, N(0,1) inputs, scale 1/8, full future (window 0)."""
     w = workload.make("tiny")
