@@ -103,14 +103,14 @@ def test_matches_oracle(case):
 
 
 def test_runs_of_several_tiles_with_ragged_ends():
-    """B=4, 32 query / 8 KV heads, T=8092: 127 query tiles of 64 per group and 32
-    groups, so each workgroup takes a run of 3 consecutive tiles (the last run holds
-    one) and rebuilds its key lists incrementally from tile to tile; the last tile
-    has 28 queries. Rows of the first run, around a run boundary and of the last
-    tile, every head of every group."""
-    T = 8092
-    rows = np.r_[0:3, 60:70, 127:130, 189:195, 62 * 64 - 3:63 * 64 + 3, 126 * 64 - 2:T]
-    _run_case(4, 32, 8, T, 128, 4, 256, 512, seed=21, rows=rows)
+    """B=1, 32 query / 8 KV heads, T=20000: 313 query tiles of 64 per group (the last
+    with 32 queries). Runs take at least T / 8192 tiles, so each workgroup takes a run
+    of 3 consecutive tiles (the last run holds one) and rebuilds its key lists
+    incrementally from tile to tile. Rows of the first run, around a later run
+    boundary and of the last tile, every head of every group."""
+    T = 20000
+    rows = np.r_[0:3, 60:70, 127:130, 189:195, 156 * 64 - 3:156 * 64 + 3, 312 * 64 - 2:T]
+    _run_case(1, 32, 8, T, 128, 4, 256, 512, seed=21, rows=rows)
 
 
 def test_sink_bias():
