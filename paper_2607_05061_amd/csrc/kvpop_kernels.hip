@@ -423,10 +423,10 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
 // NSUB key subtiles of 16 (WK = 16 NSUB keys) whose K rows stay in registers as the
 // B operand of v_mfma_f32_16x16x32_bf16. The workgroup sweeps the query tiles of 32
 // rows that can see its keys from the last one down; one step stages the tiles of
-// GC query heads of the group in LDS together with their LSE values, and every wave
-// reads them all. Descending order keeps the key blocks of one KV head -- which all
-// end at the last query row -- on the same tile at the same time, so they share it
-// through L2.
+// GC query heads of the group (two consecutive tiles when GC = 1) in LDS together
+// with their LSE values, and every wave reads them all. Descending order keeps the
+// key blocks of one KV head -- which all end at the last query row -- on the same
+// tile at the same time, so they share it through L2.
 //
 // MFMA 16x16x32 lane layout (checked on gfx950): A row m = lane % 16 holds
 // k = 8 (lane / 16) .. +7; B column n = lane % 16 holds the same k range; the 4
