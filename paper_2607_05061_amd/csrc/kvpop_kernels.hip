@@ -136,16 +136,22 @@ struct Tile16 {
 // bound; a sum that gets there from smaller terms only costs a redo. The result is
 // the same LSE; the common path costs one fma, one exp and one add per pair.
 // ---------------------------------------------------------------------------
-template <int D, int P, bool HAS_BIAS, int NQ>
-__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2))) void
+// NW waves per workgroup: 4 (one per SIMD, two workgroups per CU), or 8 with NQ = 2
+// (two per SIMD, each holding half of a 4-wave workgroup's columns; at most 128
+// VGPRs, so that two such workgroups still share a CU).
+template <int D, int P, bool HAS_BIAS, int NQ, int NW>
+__global__ __attribute__((amdgpu_flat_work_group_size(64 * NW, 64 * NW),
+                          amdgpu_waves_per_eu(NW == 8 ? 4 : 2, NW == 8 ? 4 : 2))) void
 row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const float* __restrict__ bias,
                float* __restrict__ lse, int B, int Hq, int Hkv, int T, float c, float inv_scale, int nqb, int xg,
                int zh) {
   static_assert(NQ == 2 || NQ == 4, "16-query column subtiles per wave");
+  static_assert(NW == 4 || (NW == 8 && NQ == 2), "4 waves, or 8 waves of 2 subtiles");
   constexpr int KT = 4;   // 32-key tiles per step
   using TL = Tile16<D>;
   constexpr int KS4 = TL::KS4;
-  constexpr int SPH = 4 * NQ / P;  // column subtiles per head
+  constexpr int NPW = TL::PLANES * KT / NW;  // LDS planes each wave copies per step
+  constexpr int SPH = NW * NQ / P;  // column subtiles per head
   static_assert(SPH >= 1, "at least one subtile per head");
   constexpr int BQ = 16 * SPH;
   constexpr int NV = 2 * 4 * NQ;        // values per lane and key tile
@@ -218,11 +224,13 @@ row_lse_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, c
   const int voff0 = TL::lane_voffset(lane, 0), voff1 = TL::lane_voffset(lane, 1);
   float stb = 0.f;  // raw bias of this thread's key row of the next step
   auto issue = [&](int s, uint16_t* sk) __attribute__((always_inline)) {
-    const int idx = s * KT + w;
+    // Wave w copies planes (w / KT) NPW .. of key tile w % KT of the step.
+    const int wt = NW == KT ? w : w % KT;
+    const int idx = s * KT + wt;
     if (idx < nkt) {
       const int t0 = tile_of(idx) * 32;
-      TL::template planes_to_lds<TL::PLANES>(sk + w * TL::ELEMS, Kbh + (size_t)t0 * D, min(32, T - t0), 0, voff0,
-                                             voff1);
+      TL::template planes_to_lds<NPW>(sk + wt * TL::ELEMS, Kbh + (size_t)t0 * D, min(32, T - t0),
+                                      NW == KT ? 0 : (w / KT) * NPW, voff0, voff1);
     }
     if (HAS_BIAS && tid < KT * 32) {
       const int idx2 = s * KT + (tid >> 5);
@@ -1012,9 +1020,9 @@ int stream_cus(void* stream) {
   return n;
 }
 
-template <int D, int P, bool HB, int NQ>
+template <int D, int P, bool HB, int NQ, int NW>
 int launch_p1_q(const Launch& L) {
-  constexpr int BQ = 64 * NQ / P;
+  constexpr int BQ = 16 * NW * NQ / P;
   const int G = L.Hq / L.Hkv;
   const int nqb = (L.T + BQ - 1) / BQ;
   const long long per = (long long)L.B * L.Hkv * (G / P);
@@ -1029,25 +1037,29 @@ int launch_p1_q(const Launch& L) {
   // about 33 key steps instead of 48.
   const int ncu = stream_cus(L.stream);
   const int zh = xg == 0 && grid > ncu && grid <= 2LL * ncu && ncu % per == 0 ? ncu : 0;
-  hipLaunchKernelGGL((row_lse_kernel<D, P, HB, NQ>), dim3((unsigned)grid), dim3(256), 0, (hipStream_t)L.stream,
+  hipLaunchKernelGGL((row_lse_kernel<D, P, HB, NQ, NW>), dim3((unsigned)grid), dim3(64 * NW), 0, (hipStream_t)L.stream,
                      reinterpret_cast<const uint16_t*>(L.q), reinterpret_cast<const uint16_t*>(L.k), L.bias, L.out,
                      L.B, L.Hq, L.Hkv, L.T, c, 1.0f / L.scale, nqb, xg, zh);
   return (int)hipGetLastError();
 }
 
-// A grid of full-height blocks (NQ = 4) that fits on the CUs one workgroup each
-// takes half-height blocks instead (NQ = 2; P = 8 keeps 4): twice the workgroups,
-// and the heaviest block, whose sweep sets the time when every workgroup starts at
-// once, has half the work (B = 1, T = 2048: 0.042 -> 0.031 ms). With more blocks
-// the full-height form is faster (B = 1, T = 4096: 0.090 against 0.097 ms).
+// Small grids, by the number of full-height blocks (NQ = 4; P = 8 keeps that form):
+//  * at most one per CU: half-height blocks (NQ = 2, 4 waves), twice the workgroups,
+//    and the heaviest block, whose sweep sets the time when every workgroup starts
+//    at once, has half the work (B = 1, T = 2048: 0.042 -> 0.031 ms);
+//  * up to two per CU: full-height blocks as 8 waves of 2 subtiles, two waves per
+//    SIMD, so that the heaviest block's MFMA and VALU work overlap even when it has
+//    its CU to itself (B = 1, T = 4096: 0.087-0.092 -> 0.084 ms).
 template <int D, int P, bool HB>
 int launch_p1(const Launch& L) {
   const int G = L.Hq / L.Hkv;
   const long long grid4 = (long long)((L.T + 256 / P - 1) / (256 / P)) * L.B * L.Hkv * (G / P);
   if constexpr (P < 8) {
-    if (grid4 <= stream_cus(L.stream)) return launch_p1_q<D, P, HB, 2>(L);
+    const int ncu = stream_cus(L.stream);
+    if (grid4 <= ncu) return launch_p1_q<D, P, HB, 2, 4>(L);
+    if (grid4 <= 2LL * ncu) return launch_p1_q<D, P, HB, 2, 8>(L);
   }
-  return launch_p1_q<D, P, HB, 4>(L);
+  return launch_p1_q<D, P, HB, 4, 4>(L);
 }
 
 template <int D, int P>

@@ -175,11 +175,11 @@ def test_logits_far_above_the_diagonal_reference(T, D):
                          ids=lambda s: "B%dHq%dHkv%dT%d" % s)
 def test_pass1_block_forms(shape):
     """Pass 1 has four launch forms, by grid size (P = 4 query heads per workgroup,
-    blocks of 64 NQ / P queries, 256 CUs):
-      B=1, 32/8, T=2048: 256 full-height blocks fit on the CUs one each, so NQ = 2
-        (512 half-height blocks), and the grid holds two per CU: heavy and light
-        blocks paired on each CU;
-      B=1, 32/8, T=4096: NQ = 4, 512 blocks, paired;
+    full-height blocks of 64 queries, 256 CUs):
+      B=1, 32/8, T=2048: 256 full-height blocks fit on the CUs one each, so 512
+        half-height blocks (NQ = 2, 4 waves), and the grid holds two per CU: heavy
+        and light blocks paired on each CU;
+      B=1, 32/8, T=4096: 512 full-height blocks as 8 waves of 2 subtiles, paired;
       B=8, 8/2, T=4100: NQ = 4, 1040 blocks, heaviest first;
       B=9, 8/2, T=4100: NQ = 4, 1170 blocks, heaviest first, a grid that is not a
         multiple of the workgroups per CU.

@@ -48,7 +48,8 @@ def _case(i: int):
 FIXED = [
     # pass 1: 32-query blocks (256 full-height blocks would fit one per CU), paired on CUs
     dict(B=1, Hq=32, Hkv=8, T=1500, D=128, bands=[(0, -1)], bias="none", seed=31),
-    # pass 1: full-height blocks, 376 of them, paired on CUs; pass 2 with one head per step
+    # pass 1: 376 full-height blocks as 8 waves of 2 subtiles, paired on CUs; pass 2 with
+    # one head per step
     dict(B=1, Hq=32, Hkv=8, T=3000, D=128, bands=[(0, -1), (1, 1000)], bias="random", seed=32),
     # pass 2: odd tile counts per key block with two-tile steps (G = 1), a short band
     dict(B=2, Hq=3, Hkv=3, T=1057, D=64, bands=[(3, 70)], bias="masked_large", seed=33),
