@@ -41,8 +41,10 @@
  *    [B, Hq, T] holding the linear (not log) unnormalised future mass. Keys whose
  *    band is empty (t + window > T - 1) get exactly 0.
  *  - All pointers are device pointers that the caller allocates and owns; the
- *    library allocates nothing and keeps no state between calls. Every base
- *    pointer must be 16-byte aligned. Outputs are fully overwritten (no
+ *    library allocates nothing (kvpop_running_topk_noalloc keeps a static device
+ *    array, described there) and between calls keeps only a per-device cache of
+ *    the compute-unit count, which sets the launch shape of small problems. Every
+ *    base pointer must be 16-byte aligned. Outputs are fully overwritten (no
  *    pre-zeroing needed) and must not alias any input or each other.
  *  - `stream` is a hipStream_t passed as void* (NULL = the default stream). Every
  *    call only enqueues work: it returns once the kernels are launched, and the
