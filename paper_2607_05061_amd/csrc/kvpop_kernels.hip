@@ -119,11 +119,11 @@ struct Tile16 {
 // Pass 1: row log-normaliser.
 //
 // Workgroup = (batch b, KV head h, head chunk pc of P query heads, query block of
-// BQ = 64 NQ / P positions). Its 4 waves x NQ column subtiles of 16 (head, query)
-// columns keep their Q rows in registers as the B operand of
+// BQ = 16 NW NQ / P positions). Its NW waves x NQ column subtiles of 16 (head,
+// query) columns keep their Q rows in registers as the B operand of
 // v_mfma_f32_16x16x32_bf16. One step streams KT = 4 key tiles of 32 rows through
-// LDS (wave w copies tile w), shared by all P heads. A lane holds, per key tile, 8
-// key rows (2 key subtiles x 4) of each of its NQ query columns.
+// LDS (each wave copies all or half of one), shared by all P heads. A lane holds,
+// per key tile, 8 key rows (2 key subtiles x 4) of each of its NQ query columns.
 //
 // Normalisation: every lane keeps, per query column, a reference maximum m (log2
 // units) and sum = sum exp2(x - m) over its rows of each tile. Key tiles are
@@ -712,7 +712,7 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
         float ts[NSUB];
         float y[NV], x[NV];
         const float(&pnl)[8] = nl[(g + 1) & 1];  // unit g - 1's normalisers
-        // value v of head g - 1: key subtile v % NSUB, row slot v / NSUB = 4 qs + r
+        // value v of unit g - 1: key subtile v % NSUB, row slot v / NSUB = 4 qs + r
         auto val = [&](int v) __attribute__((always_inline)) {
           const int n = v % NSUB, rr = v / NSUB;
           return __builtin_fmaf(acc_prev[rr >> 2][n][rr & 3], c, pnl[rr]);
