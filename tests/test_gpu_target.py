@@ -91,10 +91,27 @@ def test_scores_full_size_sampled():
     """T=32768 benchmark workload: the last 48 keys of two KV heads (all 4 query
     heads each) against the oracle's columns."""
     w = workload.make("qwen3_8b_t32k")
-    got, _, _ = _scores(w, 0, -1, "max", 1e-8, True)
+    got, out, mass = _scores(w, 0, -1, "max", 1e-8, True, write_mass=True)
+    # the fused and plain launches sum every key's terms in one order
+    np.testing.assert_array_equal(out, mass)
     cols = list(range(w.T - 48, w.T))
     for b, h in [(0, 2), (3, 7)]:
         m = np.stack([oracle.future_mass_columns(w.q_bits[b, h * 4 + g], w.k_bits[b, h], w.scale, cols)
                       for g in range(4)])
         r = np.log(m.max(axis=0) + 1e-8) - np.log(np.maximum(1, w.T - np.array(cols)))
         assert np.max(np.abs(got[b, h, cols] - r)) <= ABS
+
+
+def test_scores_one_batch_row_full_length():
+    """B = 1, T = 32768: plain pass 2 spreads each key block's query heads over two
+    workgroups, the fused launch keeps them in one. Both sum each key's terms in the
+    same order (bit for bit), and keys of the last key blocks match the oracle's
+    columns."""
+    w = workload.make("qwen3_8b_t32k", B=1)
+    _, out, mass = _scores(w, 0, -1, "mean", 1e-8, True, write_mass=True)
+    np.testing.assert_array_equal(out, mass)
+    cols = [32000, 32300, 32511, 32512] + list(range(w.T - 8, w.T))
+    for qh in (5, 26):
+        m = oracle.future_mass_columns(w.q_bits[0, qh], w.k_bits[0, qh // 4], w.scale, cols)
+        rel = np.abs(mass[0, qh, cols] - m) / m
+        assert rel.max() <= 2e-3, "qh %d: mass max rel err %.3e" % (qh, rel.max())
