@@ -35,6 +35,8 @@ KERNEL_SOURCES = {
     "future_mass_kernel": "kvpop_kernels.hip",
     "sparse_attn_fwd_kernel": "kvpop_sparse_attn.hip",
     "sparse_attn_fwd_kernel_exact": "kvpop_sparse_attn.hip",
+    "topk_chunk_sort_kernel": "kvpop_topk.hip",
+    "topk_merge_rank_kernel": "kvpop_topk.hip",
     "topk_prepare_kernel": "kvpop_topk.hip",
     "topk_query_kernel": "kvpop_topk.hip",
     "topk_evict_kernel": "kvpop_topk.hip",

@@ -14,11 +14,14 @@
 // every query is answered independently: E(q) is a prefix of the positions s, s+1,
 // ..., so cutoff_q is the k-th smallest value of a prefix of the array
 // A_i = rank_{s+i}, which a wavelet matrix over A answers in ceil(log2 T) constant-
-// time steps. One workgroup per sequence builds the ranks (a stable LSD radix sort
-// of 32-bit priority keys, 8 bits per pass) and the wavelet matrix (one stable
-// partition per bit level, most significant first), moving 1024 consecutive
-// elements per round so that every global access is coalesced; then one thread per
-// query walks the levels.
+// time steps. The ranks come from chunks of 4096 positions, each sorted by one
+// workgroup (a stable LSD radix sort of 32-bit priority keys, 8 bits per pass),
+// and then merged: a key's rank is its rank in its own chunk plus, for every other
+// chunk, the number of that chunk's keys ordered before it (a binary search), so
+// a sequence of 32768 positions keeps 8 workgroups busy in each step. One workgroup
+// per sequence then builds the wavelet matrix (one stable partition per bit level,
+// most significant first), moving 1024 consecutive elements per round so that every
+// global access is coalesced; then one thread per query walks the levels.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -52,6 +55,14 @@ __device__ __forceinline__ float static_priority(float r, float t, float lg) {
   return r - d;
 }
 
+// Workgroup barrier after this wave's LDS operations have completed (lgkmcnt(0)),
+// without waiting for its outstanding global stores as __syncthreads() does: for
+// barriers that only exchange LDS data.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt at their maxima
+  asm volatile("s_barrier" ::: "memory");
+}
+
 // Exclusive scan (sum or max) over the 1024 threads of the block. `sh` needs
 // kPrepWaves + 1 ints. Returns the exclusive prefix; `total` gets the reduction.
 template <bool MAX>
@@ -64,7 +75,7 @@ __device__ __forceinline__ int block_scan(int v, int* sh, int& total) {
     if (lane >= off) x = MAX ? max(x, y) : x + y;
   }
   if (lane == 63) sh[wid] = x;
-  __syncthreads();
+  lds_barrier();
   if (wid == 0) {
     int s = lane < kPrepWaves ? sh[lane] : (MAX ? INT32_MIN : 0);
     int incl = s;
@@ -75,25 +86,41 @@ __device__ __forceinline__ int block_scan(int v, int* sh, int& total) {
     }
     if (lane < kPrepWaves) sh[lane] = incl;
   }
-  __syncthreads();
+  lds_barrier();
   const int before_wave = wid > 0 ? sh[wid - 1] : (MAX ? INT32_MIN : 0);
   const int prev = __shfl_up(x, 1);  // inclusive value of lane - 1 (all lanes take part)
   const int excl = MAX ? (lane > 0 ? max(before_wave, prev) : before_wave) : before_wave + x - v;
   total = sh[kPrepWaves - 1];
-  __syncthreads();
+  lds_barrier();
   return excl;
 }
 
-// LDS of the preparation kernel.
 constexpr int kSortJ = 4;  // elements per thread in a sort round
+// Positions per sorted chunk: one sort round of kSortJ x 1024 elements.
+constexpr int kRankChunk = kSortJ * kPrepThreads;
 
-struct PrepSmem {
+// LDS of the chunk sort.
+struct SortSmem {
   int cnt[kSortJ][kPrepWaves][256];  // per-(slot, wave) digit counts of a round (cleared after use)
   int pre[kSortJ][kPrepWaves][256];  // destinations: bucket base plus earlier (slot, wave)s
-  int base[256];                // next free slot of each bucket
-  int sh[kPrepWaves + 1];       // block_scan scratch
-  int wc[2][2][4 * kPrepWaves]; // wavelet rounds: [round parity][zeros, ones][j * 16 + wave]
-  int bitcnt[32];               // elements of A with each bit set
+  int base[256];                     // next free slot of each bucket
+  int sh[kPrepWaves + 1];            // block_scan scratch
+};
+
+// Eligible positions whose wavelet levels are built in LDS: the array A and its
+// partition, 16-bit values each (ranks below 65536). One below 2^15, so that a
+// block's zero and one counts, and their sums, pack into the halves of an int.
+constexpr int kLdsLevels = 32767;
+constexpr int kLdsBlocks = (kLdsLevels + 63) / 64;  // 64-position blocks of a level
+constexpr int kLdsPerThread = (kLdsLevels + kPrepThreads - 1) / kPrepThreads;  // 32
+
+// LDS of the wavelet build.
+struct PrepSmem {
+  int sh[kPrepWaves + 1];        // block_scan scratch
+  int wc[2][2][4 * kPrepWaves];  // wavelet rounds: [round parity][zeros, ones][j * 16 + wave]
+  int bitcnt[32];                // elements of A with each bit set
+  int blk[kLdsBlocks];           // LDS levels: (zeros << 16) | ones of each 64-position block
+  int blkpre[kLdsBlocks];        // and their exclusive prefix sums
 };
 
 // One stable counting-sort pass on the 8-bit digit at `shift` (a pass of an LSD
@@ -103,7 +130,7 @@ struct PrepSmem {
 // with eight ballots.
 __device__ __forceinline__ void sort_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin,
                                           uint32_t* __restrict__ kout, uint32_t* __restrict__ vout, int n, int shift,
-                                          PrepSmem& sm) {
+                                          SortSmem& sm) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (tid < 256) sm.base[tid] = 0;
   __syncthreads();
@@ -208,7 +235,7 @@ __device__ __forceinline__ uint32_t wavelet_level(const uint32_t* __restrict__ a
         oc[j * kPrepWaves + wave] = __popcll(ob[j]);
       }
     }
-    __syncthreads();
+    lds_barrier();
     // Exclusive scans of the 64 counts in (j, wave) order, one count per lane.
     int zi = zc[lane], oi = oc[lane];
 #pragma unroll
@@ -244,8 +271,83 @@ __device__ __forceinline__ uint32_t wavelet_level(const uint32_t* __restrict__ a
     bw[W] = 0u;
     cw[W] = (uint32_t)total_ones;
   }
-  __syncthreads();
+  __syncthreads();  // the next level reads aout
   return (uint32_t)(n - total_ones);
+}
+
+// One wavelet-matrix level for an array of at most kLdsLevels elements in LDS, the
+// same result as wavelet_level. Thread tid holds the elements 1024 e + tid of all 32
+// slots e in registers, so the level needs one scan, over the zero and one counts of
+// its 64-position blocks (block 16 e + wave), instead of one per round: a pass of
+// ballots, the scan, and a pass that scatters the elements. Both passes stop at the
+// last slot that holds elements; within them the loads never branch (the buffers
+// hold 32768 entries; those from n on are ignored). Each wave gathers its 32 block
+// counts, prefixes and 64 bit words in lanes, so that each moves in one instruction.
+__device__ __forceinline__ uint32_t wavelet_level_lds(const uint16_t* __restrict__ ain, uint16_t* __restrict__ aout,
+                                                      int n, int bit, uint32_t* __restrict__ bw,
+                                                      uint32_t* __restrict__ cw, PrepSmem& sm) {
+  constexpr int E = kLdsPerThread;  // 32 slots of 1024 positions
+  static_assert(2 * E == 64, "two bit words per slot fill a wave");
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int W = (n + 31) / 32;
+  const uint64_t lt = (1ull << lane) - 1ull;
+  uint32_t x[E];
+  int cntv = 0;  // lane e: (zeros << 16) | ones of slot e's block
+  // An opaque copy of n: the 32 compares against it are then made at every level,
+  // not hoisted out of the level loop as 32 masks that spill.
+  int n1 = n;
+  asm volatile("" : "+s"(n1));
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    if (e * kPrepThreads >= n1) break;  // slots past the array (a scalar branch)
+    const int i = e * kPrepThreads + tid;
+    x[e] = ain[i];
+    const bool valid = i < n1, one = valid && ((x[e] >> bit) & 1u);
+    const uint64_t ob = __builtin_amdgcn_ballot_w64(one);
+    const uint64_t zb = __builtin_amdgcn_ballot_w64(valid) & ~ob;
+    const int packed = (__popcll(zb) << 16) | __popcll(ob);
+    cntv = lane == e ? packed : cntv;
+  }
+  if (lane < E) sm.blk[16 * lane + wave] = cntv;  // blocks past n count nothing
+  lds_barrier();
+  int tot;
+  const int ex = block_scan<false>(tid < kLdsBlocks ? sm.blk[tid] : 0, sm.sh, tot);
+  if (tid < kLdsBlocks) sm.blkpre[tid] = ex;
+  lds_barrier();
+  const int zeros = tot >> 16, ones = tot & 0xFFFF;
+  const int prev = lane < E ? sm.blkpre[16 * lane + wave] : 0;  // lane e: slot e's prefix
+  uint32_t wv = 0u, cv = 0u;  // lane 2 e + h: word h of slot e's block and the ones before it
+  // The ballots are taken again rather than kept: held across the scan, the 64
+  // masks would spill. (Opaque copies of bit and n keep the compiler from reusing
+  // the first pass's masks.)
+  int bit2 = bit, n2 = n;
+  asm volatile("" : "+s"(bit2), "+s"(n2));
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    if (e * kPrepThreads >= n2) break;
+    const int i = e * kPrepThreads + tid;
+    const bool valid = i < n2, one = valid && ((x[e] >> bit2) & 1u);
+    const uint64_t ob = __builtin_amdgcn_ballot_w64(one);
+    const uint64_t zb = __builtin_amdgcn_ballot_w64(valid) & ~ob;
+    const int pre = __builtin_amdgcn_readlane(prev, e);
+    const int zpre = pre >> 16, opre = pre & 0xFFFF;
+    if (valid) aout[one ? zeros + opre + __popcll(ob & lt) : zpre + __popcll(zb & lt)] = (uint16_t)x[e];
+    const uint32_t lo = (uint32_t)ob;
+    wv = lane == 2 * e ? lo : (lane == 2 * e + 1 ? (uint32_t)(ob >> 32) : wv);
+    cv = lane == 2 * e ? (uint32_t)opre : (lane == 2 * e + 1 ? (uint32_t)(opre + __popc(lo)) : cv);
+  }
+  // Lane 2 e + h writes word 2 (16 e + wave) + h; words from W on belong to no block.
+  const int wd = 2 * (16 * (lane >> 1) + wave) + (lane & 1);
+  if (wd < W) {
+    bw[wd] = wv;
+    cw[wd] = cv;
+  }
+  if (tid == 0) {
+    bw[W] = 0u;
+    cw[W] = (uint32_t)ones;
+  }
+  lds_barrier();  // the next level reads aout
+  return (uint32_t)zeros;
 }
 
 struct SegWork {
@@ -276,88 +378,202 @@ __device__ __forceinline__ SegWork seg_work(void* ws, size_t per_seg_words, int 
   return s;
 }
 
-// One workgroup per sequence: priorities, ranks, sorted positions, prefix maxima
-// and the wavelet matrix over A_i = rank_{s+i}.
-__global__ __launch_bounds__(kPrepThreads) void topk_prepare_kernel(const float* __restrict__ scores,
-                                                                    const float* __restrict__ log_gamma, int H,
-                                                                    int T, int s, int L, void* ws,
-                                                                    size_t per_seg_words, int32_t* __restrict__ rank) {
-  __shared__ PrepSmem sm;
+// One workgroup per (sequence, chunk of kRankChunk positions): the chunk's priority
+// keys and positions, sorted by key in place in ka / va. The sort is stable and the
+// positions enter in order, so equal keys stay in position order.
+__global__ __launch_bounds__(kPrepThreads) void topk_chunk_sort_kernel(const float* __restrict__ scores,
+                                                                       const float* __restrict__ log_gamma, int H,
+                                                                       int T, int L, void* ws, size_t per_seg_words) {
+  __shared__ SortSmem sm;
   const int tid = threadIdx.x;
-  const int seg = blockIdx.x;
+  const int nch = (T + kRankChunk - 1) / kRankChunk;
+  const int seg = (int)blockIdx.x / nch, c = (int)blockIdx.x - seg * nch;
   const int h = seg % H;
   SegWork w = seg_work(ws, per_seg_words, seg, T, L);
   const float lg = log_gamma ? log_gamma[h] : 0.f;
   const float* r = scores + (size_t)seg * T;
-  int32_t* rk = rank + (size_t)seg * T;
-  int32_t* ps = w.ps;
+  const int t0 = c * kRankChunk, n = min(kRankChunk, T - t0);
 
   for (int i = tid; i < kSortJ * kPrepWaves * 256; i += kPrepThreads) (&sm.cnt[0][0][0])[i] = 0;
   // Keys and positions; no fma contraction, to match fl(r - fl(t * lg)).
-  for (int t = tid; t < T; t += kPrepThreads) {
+  for (int i = tid; i < n; i += kPrepThreads) {
+    const int t = t0 + i;
     w.ka[t] = desc_key(static_priority(r[t], (float)t, lg));
     w.va[t] = (uint32_t)t;
   }
   __syncthreads();
+  sort_pass(w.ka + t0, w.va + t0, w.kb + t0, w.vb + t0, n, 0, sm);
+  sort_pass(w.kb + t0, w.vb + t0, w.ka + t0, w.va + t0, n, 8, sm);
+  sort_pass(w.ka + t0, w.va + t0, w.kb + t0, w.vb + t0, n, 16, sm);
+  sort_pass(w.kb + t0, w.vb + t0, w.ka + t0, w.va + t0, n, 24, sm);
+}
 
-  // Stable LSD radix sort, 8 bits per pass: equal keys keep position order.
-  sort_pass(w.ka, w.va, w.kb, w.vb, T, 0, sm);
-  sort_pass(w.kb, w.vb, w.ka, w.va, T, 8, sm);
-  sort_pass(w.ka, w.va, w.kb, w.vb, T, 16, sm);
-  sort_pass(w.kb, w.vb, w.ka, w.va, T, 24, sm);
-  // va now lists positions by rank.
-  for (int i = tid; i < T; i += kPrepThreads) {
-    const int t = (int)w.va[i];
-    ps[i] = t;
-    rk[t] = i;
+// One workgroup per (sequence, chunk): the rank of each of the chunk's keys (the
+// descending priority order, ties to the earlier position) is its index in the
+// sorted chunk plus, for every other chunk, the number of that chunk's keys ordered
+// before it. An earlier chunk holds only earlier positions, so its equal keys count;
+// a later chunk's do not. Writes rank[t] and the positions in rank order (ps).
+// Chunks are staged in LDS kMergeGroup at a time, their loads all in flight at once.
+constexpr int kMergeGroup = 8;
+__global__ __launch_bounds__(kPrepThreads) void topk_merge_rank_kernel(int T, int L, void* ws, size_t per_seg_words,
+                                                                       int32_t* __restrict__ rank) {
+  __shared__ uint32_t other[kMergeGroup][kRankChunk];
+  const int tid = threadIdx.x;
+  const int nch = (T + kRankChunk - 1) / kRankChunk;
+  const int seg = (int)blockIdx.x / nch, c = (int)blockIdx.x - seg * nch;
+  SegWork w = seg_work(ws, per_seg_words, seg, T, L);
+  const int t0 = c * kRankChunk, n = min(kRankChunk, T - t0);
+  uint32_t key[kSortJ];
+  int rk[kSortJ];
+  bool valid[kSortJ];
+#pragma unroll
+  for (int j = 0; j < kSortJ; ++j) {
+    const int i = j * kPrepThreads + tid;
+    valid[j] = i < n;
+    key[j] = valid[j] ? w.ka[t0 + i] : 0u;
+    rk[j] = i;
   }
-  __syncthreads();
+  for (int g0 = 0; g0 < nch; g0 += kMergeGroup) {
+    __syncthreads();  // every thread is done with the previous group's keys
+    uint32_t st[kMergeGroup][kSortJ];
+#pragma unroll
+    for (int g = 0; g < kMergeGroup; ++g)
+#pragma unroll
+      for (int j = 0; j < kSortJ; ++j) {
+        const int c2 = g0 + g, i = j * kPrepThreads + tid;
+        st[g][j] = c2 < nch && c2 != c && c2 * kRankChunk + i < T ? w.ka[c2 * kRankChunk + i] : 0u;
+      }
+#pragma unroll
+    for (int g = 0; g < kMergeGroup; ++g)
+#pragma unroll
+      for (int j = 0; j < kSortJ; ++j) other[g][j * kPrepThreads + tid] = st[g][j];
+    __syncthreads();
+    for (int g = 0; g < kMergeGroup && g0 + g < nch; ++g) {
+      const int c2 = g0 + g;
+      if (c2 == c) continue;
+      const int m = min(kRankChunk, T - c2 * kRankChunk);
+      const bool earlier = c2 < c;
+      // For each key, the largest prefix of the sorted chunk whose keys all come
+      // before it; the kSortJ searches advance together, so their LDS reads overlap.
+      int pos[kSortJ] = {};
+#pragma unroll
+      for (int step = kRankChunk; step > 0; step >>= 1) {
+#pragma unroll
+        for (int j = 0; j < kSortJ; ++j) {
+          const int np = pos[j] + step;
+          const uint32_t x = other[g][min(np, m) - 1];
+          if (np <= m && (earlier ? x <= key[j] : x < key[j])) pos[j] = np;
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < kSortJ; ++j) rk[j] += pos[j];
+    }
+  }
+  int32_t* rkout = rank + (size_t)seg * T;
+#pragma unroll
+  for (int j = 0; j < kSortJ; ++j) {
+    if (valid[j]) {
+      const int t = (int)w.va[t0 + j * kPrepThreads + tid];
+      rkout[t] = rk[j];
+      w.ps[rk[j]] = t;
+    }
+  }
+}
+
+// One workgroup per sequence, after the ranks: prefix maxima and the wavelet matrix
+// over A_i = rank_{s+i}. With LDSA (at most kLdsLevels eligible positions, T <=
+// 65536) every level partitions A from one LDS buffer into the other
+// (wavelet_level_lds), and only the levels' bit words and counts go to global
+// memory.
+template <bool LDSA>
+__global__ __launch_bounds__(kPrepThreads) void topk_prepare_kernel(int T, int s, int L, void* ws,
+                                                                    size_t per_seg_words,
+                                                                    const int32_t* __restrict__ rank) {
+  __shared__ PrepSmem sm;
+  __shared__ uint16_t abuf[LDSA ? 2 : 1][LDSA ? kLdsPerThread * kPrepThreads : 1];
+  const int tid = threadIdx.x;
+  const int seg = blockIdx.x;
+  SegWork w = seg_work(ws, per_seg_words, seg, T, L);
+  const int32_t* rk = rank + (size_t)seg * T;
 
   const int n = T - s;  // eligible positions s .. T-1
   if (n <= 0) return;
 
-  // A_i = rank_{s+i} and its prefix maxima (the boundary token before saturation),
-  // one coalesced round of 1024 positions at a time; also the number of A values
-  // with each bit set, which every wavelet level needs.
-  if (tid < 32) sm.bitcnt[tid] = 0;
-  int bits[32];
+  const int W = (n + 31) / 32;
+  if constexpr (LDSA) {
+    // A_i = rank_{s+i} into LDS, coalesced.
+    for (int i = tid; i < n; i += kPrepThreads) abuf[0][i] = (uint16_t)rk[s + i];
+    lds_barrier();
+    // Prefix maxima of A (the boundary token before saturation): thread tid takes
+    // positions kLdsPerThread tid .. + kLdsPerThread - 1, and one scan of the
+    // threads' maxima gives each its running maximum before them.
+    // (The loads never branch: the buffer holds 32768 entries.)
+    const int i0 = tid * kLdsPerThread;
+    int av[kLdsPerThread];
+    int mx = INT32_MIN;
 #pragma unroll
-  for (int k = 0; k < 32; ++k) bits[k] = 0;
-  int run = INT32_MIN;
-  for (int r0 = 0; r0 < n; r0 += kPrepThreads) {
-    const int i = r0 + tid;
-    const int av = i < n ? rk[s + i] : INT32_MIN;
-    if (i < n) {
-      w.ka[i] = (uint32_t)av;
-#pragma unroll
-      for (int k = 0; k < 32; ++k) bits[k] += (av >> k) & 1;
+    for (int e = 0; e < kLdsPerThread; ++e) {
+      av[e] = i0 + e < n ? (int)abuf[0][i0 + e] : INT32_MIN;
+      mx = max(mx, av[e]);
     }
     int total;
-    const int ex = block_scan<true>(av, sm.sh, total);
-    if (i < n) w.pmax[i] = max(run, max(ex, av));
-    run = max(run, total);
-  }
-  __syncthreads();
-
+    int run = block_scan<true>(mx, sm.sh, total);
 #pragma unroll
-  for (int k = 0; k < 32; ++k) {
-    int c = bits[k];
+    for (int e = 0; e < kLdsPerThread; ++e) {
+      run = max(run, av[e]);
+      if (i0 + e < n) w.pmax[i0 + e] = run;
+    }
+    // Wavelet matrix: level l splits on bit L-1-l of the current array (stable).
+    uint16_t *ain = abuf[0], *aout = abuf[LDSA ? 1 : 0];
+    for (int l = 0; l < L; ++l) {
+      const uint32_t z = wavelet_level_lds(ain, aout, n, L - 1 - l, w.bits + (size_t)l * (W + 1),
+                                           w.cnt + (size_t)l * (W + 1), sm);
+      if (tid == 0) w.zeros[l] = z;
+      uint16_t* t0 = ain;
+      ain = aout;
+      aout = t0;
+    }
+  } else {
+    // A_i = rank_{s+i} and its prefix maxima (the boundary token before
+    // saturation), one coalesced round of 1024 positions at a time; also the number
+    // of A values with each bit set, which every wavelet level needs.
+    if (tid < 32) sm.bitcnt[tid] = 0;
+    int bits[32];
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off);
-    if ((tid & 63) == 0 && k < L) atomicAdd(&sm.bitcnt[k], c);
-  }
-  __syncthreads();
-
-  // Wavelet matrix: level l splits on bit L-1-l of the current array (stable).
-  const int W = (n + 31) / 32;
-  uint32_t *ain = w.ka, *aout = w.kb;
-  for (int l = 0; l < L; ++l) {
-    const uint32_t z = wavelet_level(ain, aout, n, L - 1 - l, sm.bitcnt[L - 1 - l], w.bits + (size_t)l * (W + 1),
-                                     w.cnt + (size_t)l * (W + 1), sm);
-    if (tid == 0) w.zeros[l] = z;
-    uint32_t* t0 = ain;
-    ain = aout;
-    aout = t0;
+    for (int k = 0; k < 32; ++k) bits[k] = 0;
+    int run = INT32_MIN;
+    for (int r0 = 0; r0 < n; r0 += kPrepThreads) {
+      const int i = r0 + tid;
+      const int av = i < n ? rk[s + i] : INT32_MIN;
+      if (i < n) {
+        w.ka[i] = (uint32_t)av;
+#pragma unroll
+        for (int k = 0; k < 32; ++k) bits[k] += (av >> k) & 1;
+      }
+      int total;
+      const int ex = block_scan<true>(av, sm.sh, total);
+      if (i < n) w.pmax[i] = max(run, max(ex, av));
+      run = max(run, total);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 32; ++k) {
+      int c = bits[k];
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off);
+      if ((tid & 63) == 0 && k < L) atomicAdd(&sm.bitcnt[k], c);
+    }
+    __syncthreads();
+    // Wavelet matrix: level l splits on bit L-1-l of the current array (stable).
+    uint32_t *ain = w.ka, *aout = w.kb;
+    for (int l = 0; l < L; ++l) {
+      const uint32_t z = wavelet_level(ain, aout, n, L - 1 - l, sm.bitcnt[L - 1 - l], w.bits + (size_t)l * (W + 1),
+                                       w.cnt + (size_t)l * (W + 1), sm);
+      if (tid == 0) w.zeros[l] = z;
+      uint32_t* t0 = ain;
+      ain = aout;
+      aout = t0;
+    }
   }
 }
 
@@ -499,9 +715,22 @@ int launch_running_topk(const TopkLaunch& L) {
   const int nseg = L.B * L.H;
   const int levels = topk_levels(L.T);
   const size_t per = topk_workspace_words_per_seq(L.T);
-  hipLaunchKernelGGL(topk_prepare_kernel, dim3(nseg), dim3(kPrepThreads), 0, (hipStream_t)L.stream, L.scores,
-                     L.log_gamma, L.H, L.T, L.sinks, levels, L.workspace, per, L.rank);
+  const long long chunks = (long long)nseg * ((L.T + kRankChunk - 1) / kRankChunk);
+  hipLaunchKernelGGL(topk_chunk_sort_kernel, dim3((unsigned)chunks), dim3(kPrepThreads), 0, (hipStream_t)L.stream,
+                     L.scores, L.log_gamma, L.H, L.T, levels, L.workspace, per);
   int e = (int)hipGetLastError();
+  if (e) return e;
+  hipLaunchKernelGGL(topk_merge_rank_kernel, dim3((unsigned)chunks), dim3(kPrepThreads), 0, (hipStream_t)L.stream,
+                     L.T, levels, L.workspace, per, L.rank);
+  e = (int)hipGetLastError();
+  if (e) return e;
+  if (L.T - L.sinks <= kLdsLevels && L.T <= 65536)
+    hipLaunchKernelGGL(topk_prepare_kernel<true>, dim3(nseg), dim3(kPrepThreads), 0, (hipStream_t)L.stream, L.T,
+                       L.sinks, levels, L.workspace, per, L.rank);
+  else
+    hipLaunchKernelGGL(topk_prepare_kernel<false>, dim3(nseg), dim3(kPrepThreads), 0, (hipStream_t)L.stream, L.T,
+                       L.sinks, levels, L.workspace, per, L.rank);
+  e = (int)hipGetLastError();
   if (e) return e;
   const long long total = (long long)nseg * L.T;
   const unsigned blocks = (unsigned)((total + 255) / 256);

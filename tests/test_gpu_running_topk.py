@@ -85,6 +85,24 @@ def test_ties_break_to_earlier_position():
         np.testing.assert_array_equal(got[n], exp[n], err_msg=n)
 
 
+def test_ties_across_sorted_chunks():
+    """Exact ties spanning the 4096-position chunks that the ranking sorts one
+    workgroup each (three whole chunks and a ragged one): every tie still breaks to the
+    earlier position, an all-equal sequence ranks by position, and -0.0 ties +0.0."""
+    rng = np.random.default_rng(8)
+    T = 3 * 4096 + 123
+    scores = (np.round(rng.standard_normal((1, 3, T)) * 2) / 2).astype(np.float32)
+    scores[0, 1] = 1.5
+    scores[0, 2, ::2] = -0.0
+    scores[0, 2, 1::2] = 0.0
+    scores[0, 2, 5000:5010] = 2.0
+    got = _run(scores, None, 4, 256, 2016)
+    exp = _expected(scores, None, 4, 256, 2016)
+    for n in ("rank", "cutoff", "label", "boundary", "evict"):
+        np.testing.assert_array_equal(got[n], exp[n], err_msg=n)
+    np.testing.assert_array_equal(got["rank"][0, 1], np.arange(T))
+
+
 def test_labels_optional():
     scores = np.random.default_rng(4).standard_normal((1, 2, 200)).astype(np.float32)
     got = _run(scores, None, 1, 4, 10, labels=False, evict=False)
