@@ -20,8 +20,10 @@
 // chunk, the number of that chunk's keys ordered before it (a binary search), so
 // a sequence of 32768 positions keeps 8 workgroups busy in each step. One workgroup
 // per sequence then builds the wavelet matrix (one stable partition per bit level,
-// most significant first), moving 1024 consecutive elements per round so that every
-// global access is coalesced; then one thread per query walks the levels.
+// most significant first): in LDS, one scan per level, when A has at most 32767
+// entries and T <= 65536; otherwise in global memory, 1024 consecutive elements per
+// round so that every access is coalesced. Then one thread per query walks the
+// levels.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>

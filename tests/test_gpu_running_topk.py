@@ -151,3 +151,23 @@ def test_long_context_t131072():
             np.testing.assert_array_equal(got[n][0, h], e[n][0, 0], err_msg=n)
         np.testing.assert_array_equal(got["label"][0, h, qs], e["label"][0, 0, qs])
         np.testing.assert_array_equal(got["boundary"][0, h, qs], e["boundary"][0, 0, qs])
+
+
+@pytest.mark.parametrize("T", [32771, 32772, 40000, 136072])
+def test_each_wavelet_build(T):
+    """The wavelet levels are built in LDS up to n = T - s = 32767 eligible positions
+    (T = 32771) and in rounds through global memory beyond (T = 32772, the first size
+    past LDS; T = 40000 and 136072, ragged last rounds). Ranks, cutoffs and eviction
+    queries of every position exactly, labels and boundaries on sampled queries."""
+    s, w, k = 4, 256, 2016
+    rng = np.random.default_rng(T)
+    scores = rng.standard_normal((1, 2, T)).astype(np.float32)
+    log_gamma = np.log(np.array([0.9999, 0.99999])).astype(np.float32)
+    got = _run(scores, log_gamma, s, w, k)
+    qs = sorted(set(rng.integers(0, T, 40).tolist()) | {0, s + w + k - 1, T - 1})
+    for h in range(2):
+        e = _expected(scores[:, h:h + 1], log_gamma[h:h + 1], s, w, k, queries=qs)
+        for n in ("rank", "cutoff", "evict"):
+            np.testing.assert_array_equal(got[n][0, h], e[n][0, 0], err_msg=n)
+        np.testing.assert_array_equal(got["label"][0, h, qs], e["label"][0, 0, qs])
+        np.testing.assert_array_equal(got["boundary"][0, h, qs], e["boundary"][0, 0, qs])
