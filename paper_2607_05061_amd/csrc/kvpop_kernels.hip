@@ -45,6 +45,7 @@
 
 #include <atomic>
 #include <type_traits>
+#include <utility>
 
 
 #include "kvpop_internal.h"
@@ -766,8 +767,10 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
 
     // Tile on a band edge. Each key subtile of the wave is classified once: outside
     // the band (skipped), inside it (summed without a mask) or across its edge (each
-    // pair masked by window <= i - j <= hz).
-    auto edge_step = [&](const uint16_t* sq, const float* sl, int i0) __attribute__((always_inline)) {
+    // pair masked by window <= i - j <= hz). NBS: the bands taken (1 while the second
+    // band lies wholly past the step, see the sweep below).
+    auto edge_step = [&](auto nbs_c, const uint16_t* sq, const float* sl, int i0) __attribute__((always_inline)) {
+      constexpr int NBS = decltype(nbs_c)::value;
 #pragma unroll
       for (int g = 0; g < U; ++g) {
         const int iu = i0 - 32 * (g % TPS);
@@ -777,8 +780,8 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
           const int dlo = iu - (jw + 16 * n + 15), dhi = iu + 31 - (jw + 16 * n);
           act[n] = !(dhi < window || dlo > hz);
           inside[n] = dlo >= window && dhi <= hz;
-          act1[n] = NB == 2 && !(dhi < window1 || dlo > hz1);
-          inside1[n] = NB == 2 && dlo >= window1 && dhi <= hz1;
+          act1[n] = NBS == 2 && !(dhi < window1 || dlo > hz1);
+          inside1[n] = NBS == 2 && dlo >= window1 && dhi <= hz1;
         }
         float nl[8];
         read_nl(sl, g, nl);
@@ -800,13 +803,13 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
             const float e = exp2_fast(__builtin_fmaf(acc[rr >> 2][rr & 3], c, nl[rr]));
             const float xv = (inside[n] || (d >= window && d <= hz)) ? e : 0.f;
             ts[rr & 1] = rr < 2 ? xv : ts[rr & 1] + xv;  // the first terms seed the sums
-            if (NB == 2) {
+            if (NBS == 2) {
               const float xv1 = (inside1[n] || (d >= window1 && d <= hz1)) ? e : 0.f;
               ts1[rr & 1] = rr < 2 ? xv1 : ts1[rr & 1] + xv1;
             }
           }
           if (act[n]) colsum[g / TPS][n] += ts[0] + ts[1];
-          if (NB == 2 && act1[n]) colsum1[g / TPS][n] += ts1[0] + ts1[1];
+          if (NBS == 2 && act1[n]) colsum1[g / TPS][n] += ts1[0] + ts1[1];
         }
       }
     };
@@ -861,19 +864,21 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
       }
     };
 
-    auto step = [&](int s, const uint16_t* sq, const float* sl, uint16_t* nsq, float* nsl) __attribute__((always_inline)) {
+    auto step = [&](auto nbs_c, int s, const uint16_t* sq, const float* sl, uint16_t* nsq, float* nsl)
+                    __attribute__((always_inline)) {
+      constexpr int NBS = decltype(nbs_c)::value;
       const bool more = s + 1 < nst;
       if (more) issue(s + 1, nsq);
       const int i0 = (qt_hi - TPS * s) * 32;
       // Differences d = i - j over this wave's keys and the step's rows.
       const int dmin = i0 - 32 * (TPS - 1) - (jw + WK - 1);
       const int dmax = i0 + 31 - jw;
-      if (NB == 1) {
+      if (NBS == 1) {
         if (dmin >= window && dmax <= hz) {
           full_step(std::integral_constant<int, 1>{}, std::false_type{}, i0, sq, sl);
         } else if (!(dmax < window || dmin > hz)) {
-          if (NSUB == 2) full_step(std::integral_constant<int, 1>{}, std::true_type{}, i0, sq, sl);
-          else edge_step(sq, sl, i0);
+          if (NSUB == 2 && NB == 1) full_step(std::integral_constant<int, 1>{}, std::true_type{}, i0, sq, sl);
+          else edge_step(std::integral_constant<int, 1>{}, sq, sl, i0);
         }
       } else {
         // Each band is outside this wave's pairs of the step, covers all of them,
@@ -885,7 +890,7 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
           else if (full0) full_step(std::integral_constant<int, 1>{}, std::false_type{}, i0, sq, sl);
           else if (full1) full_step(std::integral_constant<int, 2>{}, std::false_type{}, i0, sq, sl);
         } else {
-          edge_step(sq, sl, i0);
+          edge_step(std::integral_constant<int, 2>{}, sq, sl, i0);
         }
       }
       if (more) commit(nsl);
@@ -895,18 +900,45 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
 #pragma unroll
     for (int g = 0; g < GC; ++g)
 #pragma unroll
-      for (int n = 0; n < NSUB; ++n) {
-        colsum[g][n] = 0.f;
-        if (NB == 2) colsum1[g][n] = 0.f;
-      }
+      for (int n = 0; n < NSUB; ++n) colsum[g][n] = 0.f;
     bool bad = false;
     if (!all_exact) {
       issue(0, sq0);
       commit(sl0);
       __syncthreads();
-      for (int s = 0; s < nst; s += 2) {
-        step(s, sq0, sl0, sq1, sl1);
-        if (s + 1 < nst) step(s + 1, sq1, sl1, sq0, sl0);
+      constexpr auto one_band = std::integral_constant<int, 1>{};
+      if constexpr (NB == 1) {
+        for (int s = 0; s < nst; s += 2) {
+          step(one_band, s, sq0, sl0, sq1, sl1);
+          if (s + 1 < nst) step(one_band, s + 1, sq1, sl1, sq0, sl0);
+        }
+      } else {
+        // Two bands. The leading steps (the highest rows) whose every row lies past
+        // the second band's horizon for every key of the block take the one-band
+        // code, before the second band's sums exist (with them live from the start,
+        // register pressure made those steps 4% slower); the rest take both bands.
+        // Step s's lowest row is (qt_hi - TPS s - TPS + 1) * 32.
+        const long long x = (long long)(qt_hi - TPS + 1) * 32 - ((long long)j0 + BK - 1 + hz1) - 1;
+        const int s1 = x < 0 ? 0 : (int)min((long long)nst, x / (32 * TPS) + 1);
+        int s = 0;
+        for (; s + 1 < s1; s += 2) {
+          step(one_band, s, sq0, sl0, sq1, sl1);
+          step(one_band, s + 1, sq1, sl1, sq0, sl0);
+        }
+        if (s < s1) step(one_band, s++, sq0, sl0, sq1, sl1);
+#pragma unroll
+        for (int g = 0; g < GC; ++g)
+#pragma unroll
+          for (int n = 0; n < NSUB; ++n) colsum1[g][n] = 0.f;
+        constexpr auto two_bands = std::integral_constant<int, 2>{};
+        if ((s & 1) && s < nst) {
+          step(two_bands, s, sq1, sl1, sq0, sl0);
+          ++s;
+        }
+        for (; s < nst; s += 2) {
+          step(two_bands, s, sq0, sl0, sq1, sl1);
+          if (s + 1 < nst) step(two_bands, s + 1, sq1, sl1, sq0, sl0);
+        }
       }
       // Each of the four lane sums at most 2^62 keeps the column's sum within 2^64.
 #pragma unroll
@@ -1083,8 +1115,17 @@ int launch_p2(const Launch& L, int hs) {
   const int nkb = (L.T + BK - 1) / BK;
   const long long grid = (long long)nkb * L.B * L.Hkv;
   const float c = L.scale * kLog2e;
-  const int hz = L.horizon < 0 ? L.T : L.horizon;
-  const int hz1 = NB == 2 ? (L.horizon1 < 0 ? L.T : L.horizon1) : 0;
+  int window = L.window, hz = L.horizon < 0 ? L.T : L.horizon;
+  int window1 = L.window1, hz1 = NB == 2 ? (L.horizon1 < 0 ? L.T : L.horizon1) : 0;
+  float *out = L.out, *out1 = L.out1;
+  // Two bands: the kernel's leading one-band steps serve the band that reaches
+  // further, so that band goes first (each band's sums are formed the same way in
+  // either place).
+  if (NB == 2 && hz1 > hz) {
+    std::swap(window, window1);
+    std::swap(hz, hz1);
+    std::swap(out, out1);
+  }
   // Groups an XCD runs at a time: one when a group has at least 128 key blocks
   // (T >= 32768: fewer groups sharing the XCD's L2 means fewer Q re-reads from HBM,
   // 30 -> 21 GB per launch at B = 4, T = 32768, and a higher clock); else half of its
@@ -1099,8 +1140,8 @@ int launch_p2(const Launch& L, int hs) {
   }
   hipLaunchKernelGGL((future_mass_kernel<D, NSUB, GC, HB, EPI, NB>), dim3((unsigned)(grid * hs)), dim3(256), 0,
                      (hipStream_t)L.stream, reinterpret_cast<const uint16_t*>(L.q),
-                     reinterpret_cast<const uint16_t*>(L.k), L.bias, L.lse, L.out, L.B, L.Hq, L.Hkv, L.T, c, L.window,
-                     hz, L.scores, L.agg, L.eps, L.normalize, hs > 1 ? 0 : xgroups, hs, L.window1, hz1, L.out1);
+                     reinterpret_cast<const uint16_t*>(L.k), L.bias, L.lse, out, L.B, L.Hq, L.Hkv, L.T, c, window, hz,
+                     L.scores, L.agg, L.eps, L.normalize, hs > 1 ? 0 : xgroups, hs, window1, hz1, out1);
   return (int)hipGetLastError();
 }
 

@@ -125,6 +125,11 @@ def test_two_bands_one_sweep(shape):
             ref = oracle.future_mass(w.q_bits, w.k_bits, w.scale, w.bias, a, h, lse=lse_ref)
             _check_out(got, ref, a, "shape %s bands %s band %s" % (shape, bands, (a, h)))
             np.testing.assert_allclose(got, s1.cpu().numpy(), rtol=1e-5, atol=0)
+        # the order the bands are given in changes nothing, bit for bit
+        rev = kv.kvpop_future_attn_bands(q, k, lse, w.scale, bands[::-1], key_bias=bias)
+        torch.cuda.synchronize()
+        for o, r in zip(outs, rev[::-1]):
+            np.testing.assert_array_equal(o.cpu().numpy(), r.cpu().numpy())
 
 
 @pytest.mark.parametrize("T", [5, 130, 700])
