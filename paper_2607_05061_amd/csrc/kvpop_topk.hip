@@ -102,11 +102,15 @@ constexpr int kSortJ = 4;  // elements per thread in a sort round
 constexpr int kRankChunk = kSortJ * kPrepThreads;
 
 // LDS of the chunk sort.
+// A chunk is one round of the sort, so a destination never exceeds kRankChunk and
+// the counts fit 16 bits; that leaves room in LDS for the chunk itself.
 struct SortSmem {
-  int cnt[kSortJ][kPrepWaves][256];  // per-(slot, wave) digit counts of a round (cleared after use)
-  int pre[kSortJ][kPrepWaves][256];  // destinations: bucket base plus earlier (slot, wave)s
-  int base[256];                     // next free slot of each bucket
-  int sh[kPrepWaves + 1];            // block_scan scratch
+  uint16_t cnt[kSortJ][kPrepWaves][256];  // per-(slot, wave) digit counts of a round (cleared after use)
+  uint16_t pre[kSortJ][kPrepWaves][256];  // destinations: bucket base plus earlier (slot, wave)s
+  int base[256];                          // next free slot of each bucket
+  int sh[kPrepWaves + 1];                 // block_scan scratch
+  uint32_t key[2][kRankChunk];            // the chunk's keys and positions, sorted from one
+  uint32_t val[2][kRankChunk];            // buffer into the other by each pass
 };
 
 // Eligible positions whose wavelet levels are built in LDS: the array A and its
@@ -129,7 +133,7 @@ struct PrepSmem {
 // radix sort). A round moves 4096 elements: thread tid takes r0 + 1024 j + tid for
 // j = 0..3, each placed at base[d] + (elements of digit d in earlier (j, wave)
 // pairs of the round) + (earlier lanes of its wave with digit d), the last found
-// with eight ballots.
+// with eight ballots. n <= kRankChunk (one round; the 16-bit destinations hold it).
 __device__ __forceinline__ void sort_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin,
                                           uint32_t* __restrict__ kout, uint32_t* __restrict__ vout, int n, int shift,
                                           SortSmem& sm) {
@@ -165,7 +169,7 @@ __device__ __forceinline__ void sort_pass(const uint32_t* __restrict__ kin, cons
         mm &= bit ? bb : ~bb;
       }
       rk[j] = __popcll(mm & lt);
-      if (valid[j] && rk[j] == 0) sm.cnt[j][wave][d[j]] = __popcll(mm);
+      if (valid[j] && rk[j] == 0) sm.cnt[j][wave][d[j]] = (uint16_t)__popcll(mm);
     }
     __syncthreads();
     if (tid < 256) {
@@ -177,7 +181,7 @@ __device__ __forceinline__ void sort_pass(const uint32_t* __restrict__ kin, cons
         for (int w = 0; w < kPrepWaves; ++w) c[w] = sm.cnt[j][w][tid];
 #pragma unroll
         for (int w = 0; w < kPrepWaves; ++w) {
-          sm.pre[j][w][tid] = run;
+          sm.pre[j][w][tid] = (uint16_t)run;
           sm.cnt[j][w][tid] = 0;
           run += c[w];
         }
@@ -397,17 +401,44 @@ __global__ __launch_bounds__(kPrepThreads) void topk_chunk_sort_kernel(const flo
   const int t0 = c * kRankChunk, n = min(kRankChunk, T - t0);
 
   for (int i = tid; i < kSortJ * kPrepWaves * 256; i += kPrepThreads) (&sm.cnt[0][0][0])[i] = 0;
-  // Keys and positions; no fma contraction, to match fl(r - fl(t * lg)).
+  // Keys and positions into LDS; no fma contraction, to match fl(r - fl(t * lg)).
   for (int i = tid; i < n; i += kPrepThreads) {
     const int t = t0 + i;
-    w.ka[t] = desc_key(static_priority(r[t], (float)t, lg));
-    w.va[t] = (uint32_t)t;
+    sm.key[0][i] = desc_key(static_priority(r[t], (float)t, lg));
+    sm.val[0][i] = (uint32_t)t;
   }
   __syncthreads();
-  sort_pass(w.ka + t0, w.va + t0, w.kb + t0, w.vb + t0, n, 0, sm);
-  sort_pass(w.kb + t0, w.vb + t0, w.ka + t0, w.va + t0, n, 8, sm);
-  sort_pass(w.ka + t0, w.va + t0, w.kb + t0, w.vb + t0, n, 16, sm);
-  sort_pass(w.kb + t0, w.vb + t0, w.ka + t0, w.va + t0, n, 24, sm);
+  sort_pass(sm.key[0], sm.val[0], sm.key[1], sm.val[1], n, 0, sm);
+  sort_pass(sm.key[1], sm.val[1], sm.key[0], sm.val[0], n, 8, sm);
+  sort_pass(sm.key[0], sm.val[0], sm.key[1], sm.val[1], n, 16, sm);
+  sort_pass(sm.key[1], sm.val[1], sm.key[0], sm.val[0], n, 24, sm);
+  for (int i = tid; i < n; i += kPrepThreads) {
+    w.ka[t0 + i] = sm.key[0][i];
+    w.va[t0 + i] = sm.val[0][i];
+  }
+}
+
+// For each key, the number of keys of a sorted chunk (m of them) ordered before it:
+// those below it, and with LE (an earlier chunk) those equal to it too. The kSortJ
+// searches advance together, so that their LDS reads overlap, and never branch.
+template <bool LE>
+__device__ __forceinline__ void count_before(const uint32_t* __restrict__ sorted, int m,
+                                             const uint32_t (&key)[kSortJ], int (&rk)[kSortJ]) {
+  int pos[kSortJ];
+#pragma unroll
+  for (int j = 0; j < kSortJ; ++j) pos[j] = 0;
+#pragma unroll
+  for (int step = kRankChunk; step > 0; step >>= 1) {
+#pragma unroll
+    for (int j = 0; j < kSortJ; ++j) {
+      const int np = pos[j] + step;
+      const uint32_t x = sorted[min(np, m) - 1];
+      const bool before = LE ? x <= key[j] : x < key[j];
+      pos[j] = ((np <= m) & before) ? np : pos[j];
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kSortJ; ++j) rk[j] += pos[j];
 }
 
 // One workgroup per (sequence, chunk): the rank of each of the chunk's keys (the
@@ -454,21 +485,8 @@ __global__ __launch_bounds__(kPrepThreads) void topk_merge_rank_kernel(int T, in
       const int c2 = g0 + g;
       if (c2 == c) continue;
       const int m = min(kRankChunk, T - c2 * kRankChunk);
-      const bool earlier = c2 < c;
-      // For each key, the largest prefix of the sorted chunk whose keys all come
-      // before it; the kSortJ searches advance together, so their LDS reads overlap.
-      int pos[kSortJ] = {};
-#pragma unroll
-      for (int step = kRankChunk; step > 0; step >>= 1) {
-#pragma unroll
-        for (int j = 0; j < kSortJ; ++j) {
-          const int np = pos[j] + step;
-          const uint32_t x = other[g][min(np, m) - 1];
-          if (np <= m && (earlier ? x <= key[j] : x < key[j])) pos[j] = np;
-        }
-      }
-#pragma unroll
-      for (int j = 0; j < kSortJ; ++j) rk[j] += pos[j];
+      if (c2 < c) count_before<true>(other[g], m, key, rk);
+      else count_before<false>(other[g], m, key, rk);
     }
   }
   int32_t* rkout = rank + (size_t)seg * T;
