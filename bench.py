@@ -38,6 +38,7 @@ KERNEL_SOURCES = {
     "topk_chunk_sort_kernel": "kvpop_topk.hip",
     "topk_merge_rank_kernel": "kvpop_topk.hip",
     "topk_prepare_kernel": "kvpop_topk.hip",
+    "topk_query_lds_kernel": "kvpop_topk.hip",
     "topk_query_kernel": "kvpop_topk.hip",
     "topk_evict_kernel": "kvpop_topk.hip",
 }

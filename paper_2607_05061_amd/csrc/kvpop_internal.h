@@ -71,6 +71,8 @@ int launch_future_mass(const Launch& L);
 int launch_running_topk(const TopkLaunch& L);
 int launch_sparse_attn_fwd(SparseLaunch L);
 size_t topk_workspace_words_per_seq(int T);
+// Compute units of the device of `stream` (looked up once per device); 0 if unknown.
+int stream_cus(void* stream);
 // Device address of the no-allocation scratch array on the device of `stream`
 // (resolved once per device); 0 or a hipError_t.
 int noalloc_scratch(void* stream, void** ptr);

@@ -1037,20 +1037,6 @@ future_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
   if (EPI) write_scores();
 }
 
-// Compute units of the stream's device, looked up once per device.
-int stream_cus(void* stream) {
-  constexpr int kDevices = 64;
-  static std::atomic<int> cache[kDevices];
-  int dev = 0;
-  if (hipStreamGetDevice((hipStream_t)stream, &dev) != hipSuccess && hipGetDevice(&dev) != hipSuccess) return 0;
-  if (dev < 0 || dev >= kDevices) return 0;
-  int n = cache[dev].load(std::memory_order_relaxed);
-  if (n == 0) {
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return 0;
-    cache[dev].store(n, std::memory_order_relaxed);
-  }
-  return n;
-}
 
 template <int D, int P, bool HB, int NQ, int NW>
 int launch_p1_q(const Launch& L) {
@@ -1190,6 +1176,21 @@ int launch_p2_d(const Launch& L) {
 }
 
 }  // namespace
+
+// Compute units of the stream's device, looked up once per device.
+int stream_cus(void* stream) {
+  constexpr int kDevices = 64;
+  static std::atomic<int> cache[kDevices];
+  int dev = 0;
+  if (hipStreamGetDevice((hipStream_t)stream, &dev) != hipSuccess && hipGetDevice(&dev) != hipSuccess) return 0;
+  if (dev < 0 || dev >= kDevices) return 0;
+  int n = cache[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return 0;
+    cache[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
 
 int launch_row_lse(const Launch& L) {
   if (L.D == 64) return launch_p1_d<64>(L);

@@ -604,6 +604,47 @@ __device__ __forceinline__ int rank1(const uint32_t* bw, const uint32_t* cw, int
   return (int)cw[wd] + __popc(bw[wd] & mask);
 }
 
+// The answer to query q of a sequence: the cutoff, the label of t_new = q - w and the
+// boundary token. bits, cnt: the wavelet levels' words and ones-before counts, W1
+// per level; zeros: each level's zero count; in global memory or LDS.
+__device__ __forceinline__ void answer_query(int q, int T, int s, int w_win, int k, int L, int W1,
+                                             const uint32_t* bits, const uint32_t* cnt, const uint32_t* zeros,
+                                             const int32_t* __restrict__ ps, const int32_t* __restrict__ pmax,
+                                             const int32_t* __restrict__ rk, int& cut, int& lab, int& bnd) {
+  const long long tnew = (long long)q - w_win;
+  const long long p = tnew - s + 1;  // |E(q)|
+  cut = T;
+  lab = 0;
+  bnd = -1;
+  if (p >= 1) {
+    if (p >= k) {
+      // k-th smallest of A[0, p) by walking the wavelet levels.
+      int lo = 0, hi = (int)p, kk = k, val = 0;
+      for (int l = 0; l < L; ++l) {
+        const uint32_t* bw = bits + (size_t)l * W1;
+        const uint32_t* cw = cnt + (size_t)l * W1;
+        const int o_lo = rank1(bw, cw, lo), o_hi = rank1(bw, cw, hi);
+        const int z = (hi - o_hi) - (lo - o_lo);
+        if (kk <= z) {
+          lo -= o_lo;
+          hi -= o_hi;
+        } else {
+          kk -= z;
+          const int Z = (int)zeros[l];
+          lo = Z + o_lo;
+          hi = Z + o_hi;
+          val |= 1 << (L - 1 - l);
+        }
+      }
+      cut = val;
+      bnd = ps[cut];
+    } else {
+      bnd = ps[pmax[p - 1]];
+    }
+    lab = rk[tnew] <= cut ? 1 : -1;
+  }
+}
+
 // One thread per (sequence, query).
 __global__ __launch_bounds__(256) void topk_query_kernel(int nseg, int T, int s, int w_win, int k, int L, void* ws,
                                                          size_t per_seg_words, const int32_t* __restrict__ rank,
@@ -613,43 +654,56 @@ __global__ __launch_bounds__(256) void topk_query_kernel(int nseg, int T, int s,
   if (gid >= (long long)nseg * T) return;
   const int seg = (int)(gid / T), q = (int)(gid - (long long)seg * T);
   SegWork w = seg_work(ws, per_seg_words, seg, T, L);
-  const int32_t* rk = rank + (size_t)seg * T;
-  const int32_t* ps = w.ps;
-  const long long tnew = (long long)q - w_win;
-  const long long p = tnew - s + 1;  // |E(q)|
-  int cut = T, lab = 0, bnd = -1;
-  if (p >= 1) {
-    if (p >= k) {
-      // k-th smallest of A[0, p) by walking the wavelet levels.
-      const int n = T - s;
-      const int W1 = (n + 31) / 32 + 1;
-      int lo = 0, hi = (int)p, kk = k, val = 0;
-      for (int l = 0; l < L; ++l) {
-        const uint32_t* bw = w.bits + (size_t)l * W1;
-        const uint32_t* cw = w.cnt + (size_t)l * W1;
-        const int o_lo = rank1(bw, cw, lo), o_hi = rank1(bw, cw, hi);
-        const int z = (hi - o_hi) - (lo - o_lo);
-        if (kk <= z) {
-          lo -= o_lo;
-          hi -= o_hi;
-        } else {
-          kk -= z;
-          const int Z = (int)w.zeros[l];
-          lo = Z + o_lo;
-          hi = Z + o_hi;
-          val |= 1 << (L - 1 - l);
-        }
-      }
-      cut = val;
-      bnd = ps[cut];
-    } else {
-      bnd = ps[w.pmax[p - 1]];
-    }
-    lab = rk[tnew] <= cut ? 1 : -1;
-  }
+  const int W1 = (T - s + 31) / 32 + 1;
+  int cut, lab, bnd;
+  answer_query(q, T, s, w_win, k, L, W1, w.bits, w.cnt, w.zeros, w.ps, w.pmax, rank + (size_t)seg * T, cut, lab,
+               bnd);
   cutoff[gid] = cut;
   if (label) label[gid] = lab;
   if (boundary) boundary[gid] = bnd;
+}
+
+// Words of LDS for a sequence's wavelet levels (bit words, counts and zero counts)
+// in the query kernel below: 2 L W1 + L of them (T = 32768: 30765).
+constexpr int kQueryLdsWords = 32768;
+constexpr int kQueryPerThread = 4;
+
+// One workgroup per (sequence, 4096 queries): the sequence's levels are copied into
+// LDS once, and each thread answers 4 queries from there, so that the level walks
+// read LDS instead of global memory.
+__global__ __launch_bounds__(kPrepThreads) void topk_query_lds_kernel(int T, int s, int w_win, int k, int L,
+                                                                      void* ws, size_t per_seg_words,
+                                                                      const int32_t* __restrict__ rank,
+                                                                      int32_t* __restrict__ cutoff,
+                                                                      int32_t* __restrict__ label,
+                                                                      int32_t* __restrict__ boundary) {
+  __shared__ uint32_t wl[kQueryLdsWords];
+  constexpr int QB = kQueryPerThread * kPrepThreads;
+  const int tid = threadIdx.x;
+  const int nqb = (T + QB - 1) / QB;
+  const int seg = (int)blockIdx.x / nqb, qb = (int)blockIdx.x - seg * nqb;
+  SegWork w = seg_work(ws, per_seg_words, seg, T, L);
+  const int W1 = (T - s + 31) / 32 + 1;
+  const int lw = L * W1;
+  for (int i = tid; i < lw; i += kPrepThreads) {
+    wl[i] = w.bits[i];
+    wl[lw + i] = w.cnt[i];
+  }
+  for (int i = tid; i < L; i += kPrepThreads) wl[2 * lw + i] = w.zeros[i];
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < kQueryPerThread; ++j) {
+    const int q = qb * QB + j * kPrepThreads + tid;
+    if (q < T) {
+      int cut, lab, bnd;
+      answer_query(q, T, s, w_win, k, L, W1, wl, wl + lw, wl + 2 * lw, w.ps, w.pmax, rank + (size_t)seg * T, cut,
+                   lab, bnd);
+      const size_t gid = (size_t)seg * T + q;
+      cutoff[gid] = cut;
+      if (label) label[gid] = lab;
+      if (boundary) boundary[gid] = bnd;
+    }
+  }
 }
 
 // One thread per (sequence, token): the query at which the token leaves the mask.
@@ -735,6 +789,7 @@ int launch_running_topk(const TopkLaunch& L) {
   const int nseg = L.B * L.H;
   const int levels = topk_levels(L.T);
   const size_t per = topk_workspace_words_per_seq(L.T);
+  const long long n_elig = (long long)L.T - L.sinks;  // eligible positions s .. T-1
   const long long chunks = (long long)nseg * ((L.T + kRankChunk - 1) / kRankChunk);
   hipLaunchKernelGGL(topk_chunk_sort_kernel, dim3((unsigned)chunks), dim3(kPrepThreads), 0, (hipStream_t)L.stream,
                      L.scores, L.log_gamma, L.H, L.T, levels, L.workspace, per);
@@ -744,7 +799,7 @@ int launch_running_topk(const TopkLaunch& L) {
                      L.T, levels, L.workspace, per, L.rank);
   e = (int)hipGetLastError();
   if (e) return e;
-  if (L.T - L.sinks <= kLdsLevels && L.T <= 65536)
+  if (n_elig <= kLdsLevels && L.T <= 65536)
     hipLaunchKernelGGL(topk_prepare_kernel<true>, dim3(nseg), dim3(kPrepThreads), 0, (hipStream_t)L.stream, L.T,
                        L.sinks, levels, L.workspace, per, L.rank);
   else
@@ -754,8 +809,21 @@ int launch_running_topk(const TopkLaunch& L) {
   if (e) return e;
   const long long total = (long long)nseg * L.T;
   const unsigned blocks = (unsigned)((total + 255) / 256);
-  hipLaunchKernelGGL(topk_query_kernel, dim3(blocks), dim3(256), 0, (hipStream_t)L.stream, nseg, L.T, L.sinks,
-                     L.window, L.topk, levels, L.workspace, per, L.rank, L.cutoff, L.label, L.boundary);
+  // The query kernel with the levels in LDS when they fit and its grid (one
+  // workgroup per 4096 queries) covers every compute unit: below that, the copies
+  // into LDS cost more than they save (B = 2, T = 16384: 64 workgroups, 2% slower).
+  const long long qw1 = n_elig > 0 ? (n_elig + 31) / 32 + 1 : 0;
+  const long long qblocks = (long long)nseg * ((L.T + kQueryPerThread * kPrepThreads - 1) /
+                                               (kQueryPerThread * kPrepThreads));
+  const int ncu = stream_cus(L.stream);
+  if (n_elig > 0 && 2 * levels * qw1 + levels <= kQueryLdsWords && ncu > 0 && qblocks >= ncu) {
+    hipLaunchKernelGGL(topk_query_lds_kernel, dim3((unsigned)qblocks), dim3(kPrepThreads), 0, (hipStream_t)L.stream,
+                       L.T, L.sinks, L.window, L.topk, levels, L.workspace, per, L.rank, L.cutoff, L.label,
+                       L.boundary);
+  } else {
+    hipLaunchKernelGGL(topk_query_kernel, dim3(blocks), dim3(256), 0, (hipStream_t)L.stream, nseg, L.T, L.sinks,
+                       L.window, L.topk, levels, L.workspace, per, L.rank, L.cutoff, L.label, L.boundary);
+  }
   e = (int)hipGetLastError();
   if (e || !L.evict) return e;
   hipLaunchKernelGGL(topk_evict_kernel, dim3(blocks), dim3(256), 0, (hipStream_t)L.stream, nseg, L.T, L.sinks,

@@ -171,3 +171,22 @@ def test_each_wavelet_build(T):
             np.testing.assert_array_equal(got[n][0, h], e[n][0, 0], err_msg=n)
         np.testing.assert_array_equal(got["label"][0, h, qs], e["label"][0, 0, qs])
         np.testing.assert_array_equal(got["boundary"][0, h, qs], e["boundary"][0, 0, qs])
+
+
+def test_queries_from_lds_ragged_length():
+    """64 sequences of T = 12411 (a ragged last block of queries): the query kernel
+    copies each sequence's wavelet levels into LDS once its grid covers the chip.
+    Ranks, cutoffs and eviction queries of three sequences exactly, labels and
+    boundaries on sampled queries."""
+    B, H, T, s, w, k = 8, 8, 12411, 4, 256, 2016
+    rng = np.random.default_rng(77)
+    scores = rng.standard_normal((B, H, T)).astype(np.float32)
+    log_gamma = np.log(np.linspace(0.999, 0.99999, H)).astype(np.float32)
+    got = _run(scores, log_gamma, s, w, k)
+    qs = sorted(set(rng.integers(0, T, 48).tolist()) | {0, s + w + k - 2, s + w + k - 1, T - 1})
+    for b, h in [(0, 0), (3, 5), (7, 7)]:
+        e = _expected(scores[b:b + 1, h:h + 1], log_gamma[h:h + 1], s, w, k, queries=qs)
+        for n in ("rank", "cutoff", "evict"):
+            np.testing.assert_array_equal(got[n][b, h], e[n][0, 0], err_msg=n)
+        np.testing.assert_array_equal(got["label"][b, h, qs], e["label"][0, 0, qs])
+        np.testing.assert_array_equal(got["boundary"][b, h, qs], e["boundary"][0, 0, qs])
