@@ -387,9 +387,12 @@ __device__ __forceinline__ SegWork seg_work(void* ws, size_t per_seg_words, int 
 // One workgroup per (sequence, chunk of kRankChunk positions): the chunk's priority
 // keys and positions, sorted by key in place in ka / va. The sort is stable and the
 // positions enter in order, so equal keys stay in position order.
+// With a single chunk (T <= kRankChunk) the sorted order is the ranking: the kernel
+// then writes rank[t] and the positions in rank order itself, and no merge follows.
 __global__ __launch_bounds__(kPrepThreads) void topk_chunk_sort_kernel(const float* __restrict__ scores,
                                                                        const float* __restrict__ log_gamma, int H,
-                                                                       int T, int L, void* ws, size_t per_seg_words) {
+                                                                       int T, int L, void* ws, size_t per_seg_words,
+                                                                       int32_t* __restrict__ rank) {
   __shared__ SortSmem sm;
   const int tid = threadIdx.x;
   const int nch = (T + kRankChunk - 1) / kRankChunk;
@@ -412,6 +415,14 @@ __global__ __launch_bounds__(kPrepThreads) void topk_chunk_sort_kernel(const flo
   sort_pass(sm.key[1], sm.val[1], sm.key[0], sm.val[0], n, 8, sm);
   sort_pass(sm.key[0], sm.val[0], sm.key[1], sm.val[1], n, 16, sm);
   sort_pass(sm.key[1], sm.val[1], sm.key[0], sm.val[0], n, 24, sm);
+  if (nch == 1) {
+    for (int i = tid; i < n; i += kPrepThreads) {
+      const int t = (int)sm.val[0][i];
+      rank[(size_t)seg * T + t] = i;
+      w.ps[i] = t;
+    }
+    return;
+  }
   for (int i = tid; i < n; i += kPrepThreads) {
     w.ka[t0 + i] = sm.key[0][i];
     w.va[t0 + i] = sm.val[0][i];
@@ -792,13 +803,15 @@ int launch_running_topk(const TopkLaunch& L) {
   const long long n_elig = (long long)L.T - L.sinks;  // eligible positions s .. T-1
   const long long chunks = (long long)nseg * ((L.T + kRankChunk - 1) / kRankChunk);
   hipLaunchKernelGGL(topk_chunk_sort_kernel, dim3((unsigned)chunks), dim3(kPrepThreads), 0, (hipStream_t)L.stream,
-                     L.scores, L.log_gamma, L.H, L.T, levels, L.workspace, per);
+                     L.scores, L.log_gamma, L.H, L.T, levels, L.workspace, per, L.rank);
   int e = (int)hipGetLastError();
   if (e) return e;
-  hipLaunchKernelGGL(topk_merge_rank_kernel, dim3((unsigned)chunks), dim3(kPrepThreads), 0, (hipStream_t)L.stream,
-                     L.T, levels, L.workspace, per, L.rank);
-  e = (int)hipGetLastError();
-  if (e) return e;
+  if (L.T > kRankChunk) {
+    hipLaunchKernelGGL(topk_merge_rank_kernel, dim3((unsigned)chunks), dim3(kPrepThreads), 0, (hipStream_t)L.stream,
+                       L.T, levels, L.workspace, per, L.rank);
+    e = (int)hipGetLastError();
+    if (e) return e;
+  }
   if (n_elig <= kLdsLevels && L.T <= 65536)
     hipLaunchKernelGGL(topk_prepare_kernel<true>, dim3(nseg), dim3(kPrepThreads), 0, (hipStream_t)L.stream, L.T,
                        L.sinks, levels, L.workspace, per, L.rank);
